@@ -1,0 +1,235 @@
+"""Python access to the reference oracle (``liboracle.so``, built from spice_oracle.c).
+
+TEST INFRASTRUCTURE ONLY: a plain fp64 CPU implementation of the SPICE MoE-layer
+forward, written from the paper (Sec. 2.1-2.2, 4.2, 4.3; Eq. 1, 6, 7, 9, 11).
+Only the tests, the package smoke check and the benchmark's CPU-baseline leg
+may import it.  It shares no code with the HIP library.
+
+Each wrapper passes NumPy arrays (fp32, or bf16 bits as uint16) to one C step
+and returns NumPy results; ``route`` and ``layer`` run the steps in the order
+the paper states them.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "spice_oracle.c")
+_LIB_PATH = os.environ.get("SPICE_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
+
+HIT, LORE, EXACT = 0, 1, 2
+CONF_INPUT, CONF_GATE, CONF_GATE_RENORM = 0, 1, 2
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (plain -O2, no fast-math, no FMA contraction)."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.run(["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-ffp-contract=off",
+                        "-fno-fast-math", "-Wall", "-Wextra", "-o", tmp, _SRC, "-lm"], check=True)
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build()
+        _lib = ctypes.CDLL(_LIB_PATH)
+        _declare(_lib)
+    return _lib
+
+
+class Cfg(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32), ("conf_mode", ctypes.c_int32),
+                ("tau", ctypes.c_float)]
+
+
+def make_cfg(shape, tau: float = 0.5, conf_mode: int = CONF_INPUT, norm_topk: int = 0) -> Cfg:
+    return Cfg(shape.d, shape.n_experts, shape.top_k, shape.inter, shape.shared_inter,
+               shape.lore_rank, shape.dtype, norm_topk, conf_mode, tau)
+
+
+_P = ctypes.c_void_p
+_I = ctypes.c_int32
+
+
+def _declare(L: ctypes.CDLL) -> None:
+    cp = ctypes.POINTER(Cfg)
+    L.orc_router_logits.argtypes = [cp, _I, _P, _P, _P, _P, _P]
+    L.orc_gates_topk.argtypes = [cp, _I, _P, _P, _P, _P]
+    L.orc_confidence.argtypes = [cp, _I, _P, _P, _P]
+    L.orc_classify.argtypes = [cp, _I, _P, _P, _P, _P]
+    L.orc_bucket.argtypes = [cp, _I, _P, _P, _P, _P, _P, _P]
+    L.orc_swiglu.argtypes = [_I, _I, _I, _P, _P, _P, _P]
+    L.orc_lore_delta.argtypes = [_I, _I, _I, _P, _P, _P, _P]
+    L.orc_token_output.argtypes = [cp, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    L.orc_token_output.restype = _I
+    L.orc_exact_residual.argtypes = [cp, _I, _P, _P, _P, _P, _P, _P, _P]
+    L.orc_exact_residual.restype = _I
+    L.orc_lru_step.argtypes = [_I, _I, _P, _P, _I, _I, _I, _P, _P, _I, _P, _P]
+    L.orc_lru_step.restype = _I
+
+
+def _ptr(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def _store(a: np.ndarray, dtype: int) -> np.ndarray:
+    return _c(a, np.uint16 if dtype == 1 else np.float32)
+
+
+def _table(arrs: Sequence[Optional[np.ndarray]], dtype: int):
+    keep = [None if a is None else _store(a, dtype) for a in arrs]
+    tab = (ctypes.c_void_p * len(keep))(*[None if a is None else a.ctypes.data for a in keep])
+    return tab, keep
+
+
+def router_logits(cfg: Cfg, x, wg, bias=None):
+    T = x.shape[0]
+    x, wg = _store(x, cfg.dtype), _store(wg, cfg.dtype)
+    b = None if bias is None else _c(bias, np.float32)
+    z = np.empty((T, cfg.n_experts)); zabs = np.empty((T, cfg.n_experts))
+    lib().orc_router_logits(ctypes.byref(cfg), T, _ptr(x), _ptr(wg), _ptr(b), _ptr(z), _ptr(zabs))
+    return z, zabs
+
+
+def gates_topk(cfg: Cfg, z):
+    z = _c(z, np.float64)
+    T = z.shape[0]
+    idx = np.empty((T, cfg.top_k), np.int32); g = np.empty((T, cfg.top_k))
+    probs = np.empty((T, cfg.n_experts))
+    lib().orc_gates_topk(ctypes.byref(cfg), T, _ptr(z), _ptr(idx), _ptr(g), _ptr(probs))
+    return idx, g, probs
+
+
+def confidence(cfg: Cfg, g, conf_in=None):
+    g = _c(g, np.float64)
+    T = g.shape[0]
+    ci = None if conf_in is None else _c(conf_in, np.float32)
+    conf = np.empty((T, cfg.top_k), np.float32)
+    lib().orc_confidence(ctypes.byref(cfg), T, _ptr(g), _ptr(ci), _ptr(conf))
+    return conf
+
+
+def classify(cfg: Cfg, idx, resident_mask, conf):
+    idx = _c(idx, np.int32); res = _c(resident_mask, np.int32); conf = _c(conf, np.float32)
+    cls = np.empty(idx.shape, np.uint8)
+    lib().orc_classify(ctypes.byref(cfg), idx.shape[0], _ptr(idx), _ptr(res), _ptr(conf), _ptr(cls))
+    return cls
+
+
+def bucket(cfg: Cfg, idx, cls):
+    idx = _c(idx, np.int32); cls = _c(cls, np.uint8)
+    T = idx.shape[0]
+    S = T * cfg.top_k
+    offsets = np.empty((3, cfg.n_experts + 1), np.int32)
+    perm = np.empty(S, np.int32); inv = np.empty(S, np.int32); counts = np.empty(3, np.int32)
+    lib().orc_bucket(ctypes.byref(cfg), T, _ptr(idx), _ptr(cls), _ptr(offsets), _ptr(perm), _ptr(inv),
+                     _ptr(counts))
+    return offsets, perm, inv, counts
+
+
+def swiglu(d: int, inter: int, dtype: int, w13, w2, x64):
+    w13, w2 = _store(w13, dtype), _store(w2, dtype)
+    x64 = _c(x64, np.float64); y = np.empty(d)
+    lib().orc_swiglu(d, inter, dtype, _ptr(w13), _ptr(w2), _ptr(x64), _ptr(y))
+    return y
+
+
+def lore_delta(d: int, r: int, dtype: int, A, B, x64):
+    A, B = _store(A, dtype), _store(B, dtype)
+    x64 = _c(x64, np.float64); y = np.empty(d)
+    lib().orc_lore_delta(d, r, dtype, _ptr(A), _ptr(B), _ptr(x64), _ptr(y))
+    return y
+
+
+def token_output(cfg: Cfg, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, lA, lB):
+    """Per-token layer output.  w13/w2/lA/lB: length-N sequences (None where unused)."""
+    x_row = _store(x_row, cfg.dtype)
+    idx_t = _c(idx_t, np.int32); g_t = _c(g_t, np.float64); cls_t = _c(cls_t, np.uint8)
+    t13, k1 = _table(w13, cfg.dtype); t2, k2 = _table(w2, cfg.dtype)
+    tA, k3 = _table(lA, cfg.dtype); tB, k4 = _table(lB, cfg.dtype)
+    s13, s2 = _store(w13s, cfg.dtype), _store(w2s, cfg.dtype)
+    out = np.empty(cfg.d); ys = np.empty(cfg.d); yslot = np.empty((cfg.top_k, cfg.d))
+    rc = lib().orc_token_output(ctypes.byref(cfg), _ptr(x_row), _ptr(idx_t), _ptr(g_t), _ptr(cls_t),
+                                t13, t2, _ptr(s13), _ptr(s2), tA, tB, _ptr(out), _ptr(ys), _ptr(yslot))
+    if rc != 0:
+        raise ValueError("oracle: a needed expert weight was not supplied")
+    return out, ys, yslot
+
+
+def exact_residual(cfg: Cfg, x, idx, g, cls, w13, w2):
+    T = x.shape[0]
+    x = _store(x, cfg.dtype); idx = _c(idx, np.int32); g = _c(g, np.float64); cls = _c(cls, np.uint8)
+    t13, k1 = _table(w13, cfg.dtype); t2, k2 = _table(w2, cfg.dtype)
+    resid = np.empty((T, cfg.d))
+    rc = lib().orc_exact_residual(ctypes.byref(cfg), T, _ptr(x), _ptr(idx), _ptr(g), _ptr(cls), t13, t2,
+                                  _ptr(resid))
+    if rc != 0:
+        raise ValueError("oracle: a needed expert weight was not supplied")
+    return resid
+
+
+class LRUState:
+    """Per-layer cache state: slot_expert[C], last_use[C]."""
+
+    def __init__(self, n_experts: int, C: int, initial=None):
+        self.N, self.C = n_experts, C
+        init = list(range(C)) if initial is None else list(initial)
+        self.slot_expert = np.array(init, dtype=np.int32)
+        self.last_use = np.full(C, -1, dtype=np.int32)
+
+    def step(self, step: int, idx, cls, max_admit: int):
+        idx = _c(idx, np.int32); cls = _c(cls, np.uint8)
+        T, K = idx.shape
+        adm = np.empty(max(max_admit, 1), np.int32); ev = np.empty(max(max_admit, 1), np.int32)
+        n = lib().orc_lru_step(self.N, self.C, _ptr(self.slot_expert), _ptr(self.last_use), step, T, K,
+                               _ptr(idx), _ptr(cls), max_admit, _ptr(adm), _ptr(ev))
+        return adm[:n].copy(), ev[:n].copy()
+
+    def resident_mask(self) -> np.ndarray:
+        m = np.zeros(self.N, np.int32)
+        m[self.slot_expert[self.slot_expert >= 0]] = 1
+        return m
+
+
+def route(cfg: Cfg, x, wg, bias, resident_mask, conf_in=None) -> Dict[str, np.ndarray]:
+    """Routing, gating, confidence, classification and bucketing for all tokens."""
+    z, zabs = router_logits(cfg, x, wg, bias)
+    idx, g, probs = gates_topk(cfg, z)
+    conf = confidence(cfg, g, conf_in)
+    cls = classify(cfg, idx, resident_mask, conf)
+    offsets, perm, inv, counts = bucket(cfg, idx, cls)
+    return dict(z=z, zabs=zabs, idx=idx, g=g, probs=probs, conf=conf, cls=cls, offsets=offsets,
+                perm=perm, inv_perm=inv, counts=counts)
+
+
+def layer(cfg: Cfg, x, wg, bias, resident_mask, conf_in, w13, w2, w13s, w2s, lA, lB,
+          tokens: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
+    """Whole layer: routing for all tokens, outputs for ``tokens`` (default: all)."""
+    r = route(cfg, x, wg, bias, resident_mask, conf_in)
+    T = x.shape[0]
+    toks = list(range(T)) if tokens is None else list(tokens)
+    out = np.empty((len(toks), cfg.d)); ys = np.empty((len(toks), cfg.d))
+    yslot = np.empty((len(toks), cfg.top_k, cfg.d))
+    for i, t in enumerate(toks):
+        out[i], ys[i], yslot[i] = token_output(cfg, x[t], r["idx"][t], r["g"][t], r["cls"][t],
+                                               w13, w2, w13s, w2s, lA, lB)
+    r.update(out=out, y_shared=ys, y_slot=yslot, tokens=np.array(toks, np.int32))
+    return r

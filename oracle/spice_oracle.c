@@ -1,0 +1,307 @@
+/*
+ * spice_oracle.c -- reference oracle (test infrastructure only; see spice_oracle.h).
+ *
+ * Plain loops in double precision, one step of the method per function, in the
+ * order the paper states them:
+ *   routing, Eq. 1 and Sec. 2.1            -> orc_router_logits, orc_gates_topk
+ *   hit / low-confidence / exact rule, Sec. 4.2 and 4.3 -> orc_confidence, orc_classify
+ *   grouping of slots by (class, expert)   -> orc_bucket
+ *   expert FFN, Eq. 6; LoRE, Eq. 9         -> orc_swiglu, orc_lore_delta
+ *   substitution, Eq. 7 / Eq. 11, and the gate-weighted aggregation of Sec. 2.1
+ *                                          -> orc_token_output
+ *   exact CPU path for M_cpu, Sec. 4.3     -> orc_exact_residual
+ *   expert cache bookkeeping (LRU policy)  -> orc_lru_step
+ */
+#include "spice_oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* Widen one stored element to double (exact for fp32 and bf16). */
+static double elem(const void* p, int32_t dtype, size_t i) {
+    if (dtype == ORC_BF16) {
+        uint32_t bits = (uint32_t)((const uint16_t*)p)[i] << 16;
+        float f;
+        memcpy(&f, &bits, sizeof f);
+        return (double)f;
+    }
+    return (double)((const float*)p)[i];
+}
+
+/* Eq. 1: the router maps the hidden state to one logit per routed expert. */
+void orc_router_logits(const orc_cfg_t* c, int32_t T, const void* x, const void* wg,
+                       const float* bias, double* z, double* zabs) {
+    const int32_t d = c->d, N = c->n_experts;
+    for (int32_t t = 0; t < T; ++t) {
+        for (int32_t e = 0; e < N; ++e) {
+            double acc = 0.0, mag = 0.0;
+            for (int32_t i = 0; i < d; ++i) {
+                double p = elem(x, c->dtype, (size_t)t * d + i) * elem(wg, c->dtype, (size_t)e * d + i);
+                acc += p;
+                mag += fabs(p);
+            }
+            if (bias) acc += (double)bias[e];
+            z[(size_t)t * N + e] = acc;
+            if (zabs) zabs[(size_t)t * N + e] = mag;
+        }
+    }
+}
+
+/* Eq. 1 TopK with softmax gate scores (Sec. 2.1 weighting, Sec. 4.2 gate scores). */
+void orc_gates_topk(const orc_cfg_t* c, int32_t T, const double* z, int32_t* idx, double* g,
+                    double* probs) {
+    const int32_t N = c->n_experts, K = c->top_k;
+    double* p = (double*)malloc(sizeof(double) * (size_t)N);
+    int32_t* taken = (int32_t*)malloc(sizeof(int32_t) * (size_t)N);
+    for (int32_t t = 0; t < T; ++t) {
+        const double* zt = z + (size_t)t * N;
+        /* softmax over all N experts */
+        double m = zt[0];
+        for (int32_t e = 1; e < N; ++e)
+            if (zt[e] > m) m = zt[e];
+        double s = 0.0;
+        for (int32_t e = 0; e < N; ++e) {
+            p[e] = exp(zt[e] - m);
+            s += p[e];
+        }
+        for (int32_t e = 0; e < N; ++e) p[e] /= s;
+        if (probs)
+            for (int32_t e = 0; e < N; ++e) probs[(size_t)t * N + e] = p[e];
+        /* K rounds of "largest remaining logit"; a strict '>' while scanning ids
+         * upward keeps the lower id on a tie. */
+        for (int32_t e = 0; e < N; ++e) taken[e] = 0;
+        double gsum = 0.0;
+        for (int32_t k = 0; k < K; ++k) {
+            int32_t best = -1;
+            for (int32_t e = 0; e < N; ++e) {
+                if (taken[e]) continue;
+                if (best < 0 || zt[e] > zt[best]) best = e;
+            }
+            taken[best] = 1;
+            idx[(size_t)t * K + k] = best;
+            g[(size_t)t * K + k] = p[best];
+            gsum += p[best];
+        }
+        if (c->norm_topk)
+            for (int32_t k = 0; k < K; ++k) g[(size_t)t * K + k] /= gsum;
+    }
+    free(p);
+    free(taken);
+}
+
+/* Sec. 4.2: a missing expert is judged by its routing confidence / estimated
+ * contribution.  The confidence is the caller's, or the gate score. */
+void orc_confidence(const orc_cfg_t* c, int32_t T, const double* g, const float* conf_in,
+                    float* conf) {
+    const int32_t K = c->top_k;
+    for (int32_t t = 0; t < T; ++t) {
+        double gsum = 0.0;
+        for (int32_t k = 0; k < K; ++k) gsum += g[(size_t)t * K + k];
+        for (int32_t k = 0; k < K; ++k) {
+            size_t s = (size_t)t * K + k;
+            if (c->conf_mode == ORC_CONF_INPUT)
+                conf[s] = conf_in[s];
+            else if (c->conf_mode == ORC_CONF_GATE)
+                conf[s] = (float)g[s];
+            else
+                conf[s] = (float)(g[s] / gsum);
+        }
+    }
+}
+
+/* Sec. 4.2: resident (or prefetched) -> exact on the GPU; missing with low
+ * confidence -> shared + LoRE; otherwise an exact miss (the set M of Sec. 4.3). */
+void orc_classify(const orc_cfg_t* c, int32_t T, const int32_t* idx, const int32_t* resident,
+                  const float* conf, uint8_t* cls) {
+    const int32_t K = c->top_k;
+    for (int32_t s = 0; s < T * K; ++s) {
+        if (resident[idx[s]])
+            cls[s] = ORC_HIT;
+        else if (conf[s] < c->tau) /* false for NaN */
+            cls[s] = ORC_LORE;
+        else
+            cls[s] = ORC_EXACT;
+    }
+}
+
+void orc_bucket(const orc_cfg_t* c, int32_t T, const int32_t* idx, const uint8_t* cls,
+                int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* counts) {
+    const int32_t N = c->n_experts, S = T * c->top_k;
+    int32_t* cnt = (int32_t*)calloc((size_t)3 * N, sizeof(int32_t));
+    int32_t* fill = (int32_t*)calloc((size_t)3 * N, sizeof(int32_t));
+    for (int32_t s = 0; s < S; ++s) cnt[cls[s] * N + idx[s]]++;
+    int32_t run = 0;
+    for (int32_t cl = 0; cl < 3; ++cl) {
+        int32_t start = run;
+        for (int32_t e = 0; e < N; ++e) {
+            offsets[cl * (N + 1) + e] = run;
+            run += cnt[cl * N + e];
+        }
+        offsets[cl * (N + 1) + N] = run;
+        if (counts) counts[cl] = run - start;
+    }
+    for (int32_t s = 0; s < S; ++s) {
+        int32_t key = cls[s] * N + idx[s];
+        int32_t pos = offsets[cls[s] * (N + 1) + idx[s]] + fill[key]++;
+        perm[pos] = s;
+        inv_perm[s] = pos;
+    }
+    free(cnt);
+    free(fill);
+}
+
+static double silu(double u) { return u / (1.0 + exp(-u)); }
+
+/* Eq. 6: an expert is a SwiGLU FFN, y = W2 (silu(W1 x) * (W3 x)). */
+void orc_swiglu(int32_t d, int32_t inter, int32_t dtype, const void* w13, const void* w2,
+                const double* x, double* y) {
+    double* h = (double*)malloc(sizeof(double) * (size_t)inter);
+    for (int32_t i = 0; i < inter; ++i) {
+        double a = 0.0, b = 0.0;
+        for (int32_t j = 0; j < d; ++j) {
+            a += elem(w13, dtype, (size_t)i * d + j) * x[j];
+            b += elem(w13, dtype, (size_t)(inter + i) * d + j) * x[j];
+        }
+        h[i] = silu(a) * b;
+    }
+    for (int32_t j = 0; j < d; ++j) {
+        double acc = 0.0;
+        for (int32_t i = 0; i < inter; ++i) acc += elem(w2, dtype, (size_t)j * inter + i) * h[i];
+        y[j] = acc;
+    }
+    free(h);
+}
+
+/* Eq. 9: the LoRE correction is B_e (A_e h), with A_e [r][d] and B_e [d][r]. */
+void orc_lore_delta(int32_t d, int32_t r, int32_t dtype, const void* A, const void* B,
+                    const double* x, double* delta) {
+    double* u = (double*)malloc(sizeof(double) * (size_t)(r > 0 ? r : 1));
+    for (int32_t q = 0; q < r; ++q) {
+        double acc = 0.0;
+        for (int32_t j = 0; j < d; ++j) acc += elem(A, dtype, (size_t)q * d + j) * x[j];
+        u[q] = acc;
+    }
+    for (int32_t j = 0; j < d; ++j) {
+        double acc = 0.0;
+        for (int32_t q = 0; q < r; ++q) acc += elem(B, dtype, (size_t)j * r + q) * u[q];
+        delta[j] = acc;
+    }
+    free(u);
+}
+
+int32_t orc_token_output(const orc_cfg_t* c, const void* x_row, const int32_t* idx_t,
+                         const double* g_t, const uint8_t* cls_t,
+                         const void* const* w13, const void* const* w2,
+                         const void* w13s, const void* w2s,
+                         const void* const* lA, const void* const* lB,
+                         double* out, double* ys, double* yslot) {
+    const int32_t d = c->d, K = c->top_k;
+    double* x = (double*)calloc((size_t)d, sizeof(double));
+    double* s = (double*)calloc((size_t)d, sizeof(double));
+    double* y = (double*)calloc((size_t)d, sizeof(double));
+    int32_t rc = 0;
+    for (int32_t j = 0; j < d; ++j) x[j] = elem(x_row, c->dtype, (size_t)j);
+
+    /* the always-active shared block S(x) (Sec. 2.1) */
+    orc_swiglu(d, c->shared_inter, c->dtype, w13s, w2s, x, s);
+    for (int32_t j = 0; j < d; ++j) out[j] = s[j];
+    if (ys)
+        for (int32_t j = 0; j < d; ++j) ys[j] = s[j];
+
+    for (int32_t k = 0; k < K; ++k) {
+        const int32_t e = idx_t[k];
+        const double gk = g_t[k];
+        if (cls_t[k] == ORC_LORE) {
+            /* Eq. 11: the missing expert's output is replaced by S(x) + B_e A_e x */
+            if (!lA[e] || !lB[e]) { rc = -1; break; }
+            orc_lore_delta(d, c->lore_rank, c->dtype, lA[e], lB[e], x, y);
+            for (int32_t j = 0; j < d; ++j) out[j] += gk * (s[j] + y[j]);
+        } else {
+            /* resident hit, or exact miss served with the same expert weights */
+            if (!w13[e] || !w2[e]) { rc = -1; break; }
+            orc_swiglu(d, c->inter, c->dtype, w13[e], w2[e], x, y);
+            for (int32_t j = 0; j < d; ++j) out[j] += gk * y[j];
+        }
+        if (yslot)
+            for (int32_t j = 0; j < d; ++j) yslot[(size_t)k * d + j] = y[j];
+    }
+    free(x);
+    free(s);
+    free(y);
+    return rc;
+}
+
+int32_t orc_exact_residual(const orc_cfg_t* c, int32_t T, const void* x, const int32_t* idx,
+                           const double* g, const uint8_t* cls, const void* const* w13,
+                           const void* const* w2, double* resid) {
+    const int32_t d = c->d, K = c->top_k;
+    double* xr = (double*)malloc(sizeof(double) * (size_t)d);
+    double* y = (double*)malloc(sizeof(double) * (size_t)d);
+    int32_t rc = 0;
+    for (int32_t t = 0; t < T && rc == 0; ++t) {
+        for (int32_t j = 0; j < d; ++j) {
+            xr[j] = elem(x, c->dtype, (size_t)t * d + j);
+            resid[(size_t)t * d + j] = 0.0;
+        }
+        for (int32_t k = 0; k < K; ++k) {
+            size_t s = (size_t)t * K + k;
+            if (cls[s] != ORC_EXACT) continue;
+            if (!w13[idx[s]] || !w2[idx[s]]) { rc = -1; break; }
+            orc_swiglu(d, c->inter, c->dtype, w13[idx[s]], w2[idx[s]], xr, y);
+            for (int32_t j = 0; j < d; ++j) resid[(size_t)t * d + j] += g[s] * y[j];
+        }
+    }
+    free(xr);
+    free(y);
+    return rc;
+}
+
+int32_t orc_lru_step(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t* last_use,
+                     int32_t step, int32_t T, int32_t K, const int32_t* idx, const uint8_t* cls,
+                     int32_t max_admit, int32_t* admitted, int32_t* evicted) {
+    int32_t* exact_count = (int32_t*)calloc((size_t)n_experts, sizeof(int32_t));
+    int32_t* slot_of = (int32_t*)malloc(sizeof(int32_t) * (size_t)n_experts);
+    for (int32_t e = 0; e < n_experts; ++e) slot_of[e] = -1;
+    for (int32_t sl = 0; sl < C; ++sl)
+        if (slot_expert[sl] >= 0) slot_of[slot_expert[sl]] = sl;
+
+    /* touch the experts that were hit in this step */
+    for (int32_t s = 0; s < T * K; ++s) {
+        if (cls[s] == ORC_HIT && slot_of[idx[s]] >= 0) last_use[slot_of[idx[s]]] = step;
+        if (cls[s] == ORC_EXACT) exact_count[idx[s]]++;
+    }
+
+    int32_t n_adm = 0;
+    while (n_adm < max_admit) {
+        /* next candidate: most tokens, then lowest id; never a LoRE-only miss */
+        int32_t cand = -1;
+        for (int32_t e = 0; e < n_experts; ++e) {
+            if (exact_count[e] == 0 || slot_of[e] >= 0) continue;
+            if (cand < 0 || exact_count[e] > exact_count[cand]) cand = e;
+        }
+        if (cand < 0) break;
+        /* victim: least recently used slot not used in this step, ties by expert id
+         * (an empty slot, expert -1, sorts first among equal last_use) */
+        int32_t victim = -1;
+        for (int32_t sl = 0; sl < C; ++sl) {
+            if (last_use[sl] == step) continue;
+            if (victim < 0 || last_use[sl] < last_use[victim] ||
+                (last_use[sl] == last_use[victim] && slot_expert[sl] < slot_expert[victim]))
+                victim = sl;
+        }
+        if (victim < 0) break;
+        int32_t old = slot_expert[victim];
+        if (old >= 0) slot_of[old] = -1;
+        slot_expert[victim] = cand;
+        slot_of[cand] = victim;
+        last_use[victim] = step;
+        exact_count[cand] = 0;
+        admitted[n_adm] = cand;
+        evicted[n_adm] = old;
+        ++n_adm;
+    }
+    free(exact_count);
+    free(slot_of);
+    return n_adm;
+}

@@ -1,0 +1,109 @@
+/*
+ * spice_oracle.h -- reference oracle for SPICE's per-layer MoE forward under a
+ * partial GPU expert cache (arXiv 2608.21240, Sec. 2.1-2.2, 4.2, 4.3).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This is a plain, slow CPU implementation in fp64
+ * written from the paper to check the HIP library against.  It shares no code,
+ * header, helper or table with the library; only tests, the package smoke
+ * check and the benchmark's CPU-baseline leg may load it.
+ *
+ * Storage types: every tensor argument is either fp32 (dtype 0) or bf16 bits
+ * stored as uint16 (dtype 1).  Each element is widened to double exactly and
+ * all arithmetic is done in double.
+ *
+ * All matrices are row-major with Linear's [out][in] convention:
+ *   router   Wg  [N][d]
+ *   expert   W13 [2I][d]  (rows 0..I-1 = gate W1, rows I..2I-1 = up W3), W2 [d][I]
+ *   shared   W13s[2Is][d], W2s[d][Is]
+ *   LoRE     A   [r][d],  B [d][r]          (Eq. 9)
+ * Slot id of token t's k-th routed choice = t*K + k.
+ * Parity pins: see tests/test_oracle_*.py.  No function here is unpinned.
+ */
+#ifndef SPICE_ORACLE_H
+#define SPICE_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_F32 = 0, ORC_BF16 = 1 };
+enum { ORC_HIT = 0, ORC_LORE = 1, ORC_EXACT = 2 };
+enum { ORC_CONF_INPUT = 0, ORC_CONF_GATE = 1, ORC_CONF_GATE_RENORM = 2 };
+
+typedef struct {
+    int32_t d, n_experts, top_k, inter, shared_inter, lore_rank;
+    int32_t dtype;     /* ORC_F32 / ORC_BF16 */
+    int32_t norm_topk; /* 1: divide the K selected gates by their sum */
+    int32_t conf_mode; /* ORC_CONF_* */
+    float tau;         /* confidence threshold */
+} orc_cfg_t;
+
+/* Router logits z[t][e] = sum_i x[t][i] Wg[e][i] + bias[e] (Eq. 1).  zabs (nullable)
+ * receives sum_i |x[t][i] Wg[e][i]|, the scale of the summation's rounding error. */
+void orc_router_logits(const orc_cfg_t* c, int32_t T, const void* x, const void* wg,
+                       const float* bias, double* z, double* zabs);
+
+/* Softmax over all N experts and top-K by logit (descending, ties -> lower id):
+ * idx[T][K], gate g[T][K] = softmax prob of the chosen expert (renormalised over
+ * the K when norm_topk).  probs (nullable) receives the full softmax [T][N]. */
+void orc_gates_topk(const orc_cfg_t* c, int32_t T, const double* z, int32_t* idx, double* g,
+                    double* probs);
+
+/* Per-slot confidence (fp32): caller's conf_in, the gate, or the renormalised gate. */
+void orc_confidence(const orc_cfg_t* c, int32_t T, const double* g, const float* conf_in,
+                    float* conf);
+
+/* Slot class: HIT if the expert is resident, else LORE if conf < tau, else EXACT
+ * (a NaN confidence is EXACT).  resident[e] != 0 means resident. */
+void orc_classify(const orc_cfg_t* c, int32_t T, const int32_t* idx, const int32_t* resident,
+                  const float* conf, uint8_t* cls);
+
+/* Counting sort of slot ids by key (class, expert), stable in slot order.
+ * offsets[3][N+1]: offsets[c][e] = first position of bucket (c, e); offsets[c][N] = end
+ * of class c.  perm[pos] = slot, inv_perm[slot] = pos.  counts[3] (nullable) per class. */
+void orc_bucket(const orc_cfg_t* c, int32_t T, const int32_t* idx, const uint8_t* cls,
+                int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* counts);
+
+/* One SwiGLU FFN on one token: y = W2 (silu(W1 x) * (W3 x)), x given in double. */
+void orc_swiglu(int32_t d, int32_t inter, int32_t dtype, const void* w13, const void* w2,
+                const double* x, double* y);
+
+/* LoRE correction delta = B (A x) for one token (Eq. 9). */
+void orc_lore_delta(int32_t d, int32_t r, int32_t dtype, const void* A, const void* B,
+                    const double* x, double* delta);
+
+/* Layer output of one token t (Eq. 7 and Eq. 11 inside the gate-weighted sum of
+ * Sec. 2.1):  out = S(x) + sum_{HIT,EXACT} g E_e(x) + sum_{LORE} g (S(x) + B_e A_e x).
+ * w13/w2/lA/lB are per-expert pointer tables [N]; only experts this token needs
+ * must be non-NULL.  ys (nullable) receives S(x); yslot (nullable, [K][d]) the
+ * per-slot term (E_e(x) or B_e A_e x).  Returns 0, or -1 if a needed pointer is NULL. */
+int32_t orc_token_output(const orc_cfg_t* c, const void* x_row, const int32_t* idx_t,
+                         const double* g_t, const uint8_t* cls_t,
+                         const void* const* w13, const void* const* w2,
+                         const void* w13s, const void* w2s,
+                         const void* const* lA, const void* const* lB,
+                         double* out, double* ys, double* yslot);
+
+/* Exact residual of the CPU path (Sec. 4.3): resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t).
+ * Returns 0, or -1 if a needed expert pointer is NULL. */
+int32_t orc_exact_residual(const orc_cfg_t* c, int32_t T, const void* x, const int32_t* idx,
+                           const double* g, const uint8_t* cls, const void* const* w13,
+                           const void* const* w2, double* resid);
+
+/* LRU expert-cache step for one layer at one decode step (the stack workload).
+ * State: slot_expert[C] (expert in each slot), last_use[C] (step of last use, -1 unused).
+ * HIT experts are touched; EXACT-miss experts are admission candidates ordered by
+ * (token count desc, id asc); each takes the slot of the resident expert with the
+ * smallest (last_use, expert id) not used in this step; at most max_admit.  LORE
+ * misses are never admitted.  admitted[] / evicted[] receive up to max_admit ids.
+ * Returns the number admitted. */
+int32_t orc_lru_step(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t* last_use,
+                     int32_t step, int32_t T, int32_t K, const int32_t* idx, const uint8_t* cls,
+                     int32_t max_admit, int32_t* admitted, int32_t* evicted);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
