@@ -1,0 +1,207 @@
+/*
+ * spice_moe.h -- C ABI of the SPICE MoE-layer hot path for AMD Instinct MI355X (gfx950).
+ *
+ * The library computes one Mixture-of-Experts layer under a partial GPU expert
+ * cache, as SPICE defines it (arXiv 2608.21240):
+ *   1. router logits and top-K gating                    (Eq. 1; Sec. 2.1, 2.2)
+ *   2. per-slot classification: resident hit, low-confidence miss (LoRE),
+ *      exact miss; then bucketing of slots by (class, expert)   (Sec. 4.2, 4.3)
+ *   3. grouped SwiGLU FFN of the resident experts plus the always-resident
+ *      shared block                                       (Eq. 6; Sec. 2.1, 4.2)
+ *   4. LoRE surrogate B_e A_e h for low-confidence misses (Eq. 7, 9, 11)
+ *   5. exact CPU residual for exact misses, from host weights (Sec. 4.3, M_cpu)
+ *   6. gate-weighted combine of all terms                 (Sec. 2.1; Eq. 11; Sec. 4.3 merge)
+ *
+ * Conventions for every entry point
+ *   - Plain pointers.  "device" = memory the GPU reads/writes (hipMalloc or
+ *     equivalent); "host" = CPU memory.  The caller owns every buffer, including
+ *     the workspace; the library keeps no pointer after returning (except the
+ *     cache handle, which borrows what it was created with until destroyed).
+ *   - Row-major arrays.  Weight matrices use Linear's [out][in] layout.
+ *     Expert ids are 0..N-1.  Slot id of token t's k-th choice = t*K + k.
+ *   - dtype SPICE_F32: activations and weights are fp32.  dtype SPICE_BF16:
+ *     activations and weights are bf16 (passed as raw 16-bit values); all
+ *     accumulation is fp32 (router logits: fp64).
+ *   - Device entry points check their arguments on the host, then enqueue
+ *     kernels on `stream` and return; they never synchronise.  A bad value
+ *     inside a device array (an out-of-range cache slot or expert id) never
+ *     causes an out-of-bounds access: the kernels skip it and raise a flag
+ *     in the workspace (read it with spice_workspace_flags).
+ *   - Entry points never abort or throw; they return a negative status and
+ *     leave a message for spice_last_error() (per thread).  T == 0 is a no-op
+ *     that returns SPICE_OK.
+ */
+#ifndef SPICE_MOE_H
+#define SPICE_MOE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Same type as hipStream_t; NULL selects the default stream. */
+typedef struct ihipStream_t* spice_stream_t;
+
+typedef enum {
+    SPICE_OK = 0,
+    SPICE_ERR_INVALID = -1,     /* a bad argument (NULL, out of range, overflow, aliasing) */
+    SPICE_ERR_UNSUPPORTED = -2, /* valid but not handled: size alignment, dtype, N > 256 ... */
+    SPICE_ERR_HIP = -3,         /* the HIP runtime reported an error (launch, copy, earlier fault) */
+    SPICE_ERR_WORKSPACE = -4,   /* workspace smaller than spice_workspace_bytes() */
+    SPICE_ERR_INTERNAL = -5
+} spice_status_t;
+
+enum { SPICE_F32 = 0, SPICE_BF16 = 1 };
+/* Where the per-slot routing confidence comes from (Sec. 4.2 leaves it open):
+ * the caller's array, the slot's gate score, or the gate renormalised over the K. */
+enum { SPICE_CONF_INPUT = 0, SPICE_CONF_GATE = 1, SPICE_CONF_GATE_RENORM = 2 };
+/* Slot classes (Sec. 4.2): resident or prefetched -> exact on the GPU; missing with
+ * confidence < tau -> shared + LoRE; otherwise an exact miss served on the CPU. */
+enum { SPICE_CLASS_HIT = 0, SPICE_CLASS_LORE = 1, SPICE_CLASS_EXACT = 2 };
+
+#define SPICE_MAX_EXPERTS 256
+#define SPICE_MAX_TOKENS 65536
+#define SPICE_MAX_LORE_RANK 256
+/* The first SPICE_WS_CONTROL_BYTES of a workspace hold counters and flags.
+ * They must be zero before the workspace is first used (spice_workspace_init,
+ * or any zero fill); every completed call leaves the counters zero again. */
+#define SPICE_WS_CONTROL_BYTES 65536
+
+/* Device-side flags (bit mask) raised in the workspace by a kernel that met bad data. */
+#define SPICE_FLAG_BAD_SLOT 1u   /* resident_slot[e] outside [-1, n_slots) */
+#define SPICE_FLAG_BAD_INDEX 2u  /* perm / offsets / topk_idx value out of range */
+
+typedef struct {
+    int32_t d;            /* hidden size */
+    int32_t n_experts;    /* N routed experts, 1..256 */
+    int32_t top_k;        /* K, 1..N */
+    int32_t inter;        /* I, routed SwiGLU intermediate size */
+    int32_t shared_inter; /* I_s, intermediate of the shared block (all shared experts stacked) */
+    int32_t lore_rank;    /* r of Eq. 9, 0..256 */
+    int32_t n_slots;      /* C, slots of the GPU expert pool */
+    int32_t dtype;        /* SPICE_F32 or SPICE_BF16 */
+    int32_t norm_topk;    /* 1: renormalise the K selected gates to sum 1 */
+    int32_t conf_mode;    /* SPICE_CONF_* */
+    float tau;            /* confidence threshold: LoRE iff conf < tau (NaN conf -> exact) */
+} spice_moe_cfg_t;
+
+/* Size alignment required: d, inter and shared_inter multiples of 8 (bf16) or 4 (fp32);
+ * lore_rank a multiple of 8 (bf16) or 4 (fp32). */
+
+/* Bytes of device workspace that a call with T tokens needs (every entry point below
+ * accepts the same workspace).  Returns 0 for an invalid cfg or T. */
+size_t spice_workspace_bytes(const spice_moe_cfg_t* cfg, int32_t T);
+
+/* Zero the control region of a device workspace (a fill kernel on `stream`). */
+spice_status_t spice_workspace_init(void* ws, size_t ws_bytes, spice_stream_t stream);
+
+/* Copy the device flags of a workspace to *flags (synchronises `stream`); clear them if clear != 0. */
+spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags, int32_t clear,
+                                     spice_stream_t stream);
+
+/*
+ * Steps 1-2: router logits z = x Wg^T (+ bias), softmax over all N, top-K by logit
+ * (descending, ties -> lower expert id; Eq. 1), gate g = softmax probability of the
+ * chosen expert (Sec. 2.1 weighting), per-slot confidence and class (Sec. 4.2), and a
+ * stable counting sort of slot ids by (class, expert).
+ *   x             device [T][d]      activations (dtype)
+ *   w_gate        device [N][d]      router weight (dtype)
+ *   logit_bias    device [N] fp32    added to the logits, or NULL
+ *   resident_slot device [N] int32   pool slot of expert e, or -1 when not resident
+ *   conf          device [T][K] fp32 per-slot confidence; required iff conf_mode == INPUT
+ *   logits        device [T][N] fp64 out, or NULL (logits are summed in fp64)
+ *   topk_idx      device [T][K] int32 out
+ *   topk_w        device [T][K] fp32 out, gate scores
+ *   slot_class    device [T][K] uint8 out, SPICE_CLASS_*
+ *   offsets       device [3][N+1] int32 out: offsets[c][e] = first position of bucket
+ *                 (c, e) in perm; offsets[c][N] = end of class c (classes laid out
+ *                 HIT, LORE, EXACT; inside a bucket slots keep ascending slot order)
+ *   perm          device [T*K] int32 out: perm[pos] = slot id
+ *   inv_perm      device [T*K] int32 out: inv_perm[slot] = pos
+ */
+spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                const void* w_gate, const float* logit_bias,
+                                const int32_t* resident_slot, const float* conf, double* logits,
+                                int32_t* topk_idx, float* topk_w, uint8_t* slot_class,
+                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, void* ws,
+                                size_t ws_bytes, spice_stream_t stream);
+
+/*
+ * Step 3: grouped SwiGLU FFN y = W2 (silu(W1 x) * (W3 x)) (Eq. 6) for every HIT slot,
+ * grouped by expert, plus the shared block S(x) (Sec. 2.1, 4.2) for all T tokens.
+ * When lore_A and lore_B are both non-NULL the LoRE corrections of step 4 are computed
+ * in the same launches (the same result as calling lore_surrogate_apply).
+ *   x, perm, offsets       as produced/consumed by moe_route_bucket
+ *   resident_slot device [N] int32, as in moe_route_bucket
+ *   w13_pool      device [C][2I][d]  rows 0..I-1 gate W1, rows I..2I-1 up W3 (dtype)
+ *   w2_pool       device [C][d][I]   down projection (dtype)
+ *   w13_shared    device [2I_s][d], w2_shared device [d][I_s]   (ignored if I_s == 0)
+ *   lore_A, lore_B see lore_surrogate_apply, or NULL
+ *   y_slots       device [T*K][d] fp32 out: row pos = expert output for slot perm[pos]
+ *                 (HIT rows; LORE rows too when LoRE is fused; other rows untouched)
+ *   y_shared      device [T][d] fp32 out: S(x_t)
+ */
+spice_status_t moe_expert_ffn_grouped(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                      const int32_t* perm, const int32_t* offsets,
+                                      const int32_t* resident_slot, const void* w13_pool,
+                                      const void* w2_pool, const void* w13_shared,
+                                      const void* w2_shared, const void* lore_A,
+                                      const void* lore_B, float* y_slots, float* y_shared,
+                                      void* ws, size_t ws_bytes, spice_stream_t stream);
+
+/*
+ * Step 4: LoRE correction delta = B_e (A_e x) (Eq. 9) for every LORE slot, grouped by
+ * expert.  The shared part S(x) of Eq. 11 is not recomputed: moe_combine adds it.
+ *   lore_A  device [N][r][d] (dtype), lore_B device [N][d][r] (dtype): factors of every
+ *           routed expert, always resident (Sec. 4.2)
+ *   y_slots device [T*K][d] fp32 out: LORE rows receive delta; other rows untouched
+ */
+spice_status_t lore_surrogate_apply(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                    const int32_t* perm, const int32_t* offsets,
+                                    const void* lore_A, const void* lore_B, float* y_slots,
+                                    void* ws, size_t ws_bytes, spice_stream_t stream);
+
+/*
+ * Step 6: out[t] = (1 + sum_{k in LORE(t)} g) S(x_t) + sum_{k in HIT(t)} g y
+ *                  + sum_{k in LORE(t)} g delta + resid[t]
+ * i.e. the gate-weighted sum of Sec. 2.1 with each LoRE slot's output replaced by
+ * S(x) + B_e A_e x (Eq. 11) and the CPU outputs merged in (Sec. 4.3).
+ *   topk_w, slot_class, inv_perm  device, from moe_route_bucket
+ *   y_slots device [T*K][d] fp32, y_shared device [T][d] fp32
+ *   resid   device [T][d] fp32 exact-miss residual, or NULL (treated as zero)
+ *   out     device [T][d] dtype out (bf16: round to nearest even); must not alias inputs
+ */
+spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w,
+                           const uint8_t* slot_class, const int32_t* inv_perm,
+                           const float* y_slots, const float* y_shared, const float* resid,
+                           void* out, spice_stream_t stream);
+
+/*
+ * Step 5, host side: resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t) computed on the
+ * CPU from host-resident expert weights (M_cpu of Eq. 12; Sec. 4.3: exact, the same
+ * weights, routing untouched).  Synchronous and reentrant; uses n_threads worker
+ * threads (<= 0: one per online CPU).  The result does not depend on n_threads.
+ *   x_host        host [T][d] (dtype)
+ *   topk_idx_host host [T][K] int32, topk_w_host host [T][K] fp32,
+ *   slot_class_host host [T][K] uint8
+ *   w13_host      host table [N] of pointers to [2I][d] (dtype); entries of experts with
+ *                 no EXACT slot may be NULL
+ *   w2_host       host table [N] of pointers to [d][I] (dtype)
+ *   resid_host    host [T][d] fp32 out (overwritten; zero rows for tokens with no exact slot)
+ */
+spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, int32_t T, const void* x_host,
+                                       const int32_t* topk_idx_host, const float* topk_w_host,
+                                       const uint8_t* slot_class_host,
+                                       const void* const* w13_host, const void* const* w2_host,
+                                       float* resid_host, int32_t n_threads);
+
+/* Text of a status code, and the last error message of the calling thread. */
+const char* spice_status_string(spice_status_t status);
+const char* spice_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif

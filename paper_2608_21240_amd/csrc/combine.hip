@@ -1,0 +1,77 @@
+// Gate-weighted combine (Sec. 2.1) with LoRE substitution (Eq. 11) and the merge
+// of the CPU exact residual (Sec. 4.3), plus a small fill kernel.
+//
+// One thread per 4 consecutive hidden features of one token; grid (d/1024, T).
+// out = (1 + sum_{LORE} g) * S(x) + sum_{HIT,LORE} g * y_slots[inv_perm[slot]] + resid.
+#include <hip/hip_runtime.h>
+
+#include "spice_internal.h"
+
+namespace spice {
+namespace {
+
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+template <int DT>
+__global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
+    const int t = blockIdx.y;
+    const int dim = (blockIdx.x * blockDim.x + threadIdx.x) * 4;
+    if (dim >= a.d) return;
+    const f32x4_t ys = *reinterpret_cast<const f32x4_t*>(a.y_shared + (size_t)t * a.d + dim);
+    f32x4_t acc = {0.f, 0.f, 0.f, 0.f};
+    float coef = 1.0f;
+    const int S = a.T * a.K;
+    for (int k = 0; k < a.K; ++k) {
+        const int s = t * a.K + k;
+        const uint8_t c = a.slot_class[s];
+        if (c != SPICE_CLASS_HIT && c != SPICE_CLASS_LORE) continue;
+        const int pos = a.inv_perm[s];
+        if (pos < 0 || pos >= S) continue;
+        const float g = a.topk_w[s];
+        const f32x4_t y = *reinterpret_cast<const f32x4_t*>(a.y_slots + (size_t)pos * a.d + dim);
+        acc += g * y;
+        if (c == SPICE_CLASS_LORE) coef += g;
+    }
+    f32x4_t o = coef * ys + acc;
+    if (a.resid) o += *reinterpret_cast<const f32x4_t*>(a.resid + (size_t)t * a.d + dim);
+    if (DT == SPICE_BF16) {
+        uint2 p;
+        p.x = f32_to_bf16_rne(o.x) | (f32_to_bf16_rne(o.y) << 16);
+        p.y = f32_to_bf16_rne(o.z) | (f32_to_bf16_rne(o.w) << 16);
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(a.out) + (size_t)t * a.d + dim) = p;
+    } else {
+        *reinterpret_cast<f32x4_t*>(static_cast<float*>(a.out) + (size_t)t * a.d + dim) = o;
+    }
+}
+
+__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t v) {
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+        p[i] = v;
+}
+
+}  // namespace
+
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s) {
+    dim3 grid((a.d / 4 + 255) / 256, a.T);
+    if (a.dtype == SPICE_BF16)
+        hipLaunchKernelGGL(combine_kernel<SPICE_BF16>, grid, dim3(256), 0, s, a);
+    else
+        hipLaunchKernelGGL(combine_kernel<SPICE_F32>, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t words, uint32_t value, hipStream_t s) {
+    if (words == 0) return hipSuccess;
+    const size_t blocks = (words + 255) / 256;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)(blocks < 1024 ? blocks : 1024)), dim3(256), 0, s, p,
+                       words, value);
+    return hipGetLastError();
+}
+
+}  // namespace spice

@@ -1,0 +1,305 @@
+// Router logits, softmax top-K gating, per-slot classification and (class, expert)
+// bucketing in one launch (Eq. 1; Sec. 2.1, 4.2, 4.3).
+//
+// Grid: (ceil(N/8) expert groups) x (ceil(T/8) token tiles), 256 threads.
+//   1. every block: fp64 logits of 8 tokens x 8 experts (each wave: 2 expert rows,
+//      lanes stride the hidden dimension in 16-byte chunks; bf16 x bf16 and
+//      fp32 x fp32 products are exact in fp64, so only the summation rounds);
+//   2. the last block of a token tile to finish: softmax and top-K of its tokens
+//      (one wave per token, wave-wide argmax with the lower id winning ties),
+//      gate scores, confidence and class;
+//   3. the last token tile to finish: stable counting sort of all T*K slots by
+//      key (class, expert) with per-wave histograms, a block scan, and ballot
+//      matching to rank equal keys inside each 64-slot chunk.
+// "Last block" is decided with an agent-scope atomic counter in the workspace
+// control region after a device fence; the last block resets the counter.
+#include <float.h>
+#include <limits.h>
+
+#include <hip/hip_runtime.h>
+
+#include "spice_internal.h"
+
+namespace spice {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / 64;
+constexpr int kMaxKeys = 3 * SPICE_MAX_EXPERTS;
+
+__device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) {
+    return __uint_as_float(bits16 << 16);
+}
+
+// 16-byte chunk of `n` elements widened to double.
+template <int DT>
+struct Chunk;
+
+template <>
+struct Chunk<SPICE_BF16> {
+    static constexpr int n = 8;
+    __device__ __forceinline__ static void load(const void* base, size_t elem, double* v) {
+        const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = (double)bf16_bits_to_float(w[i] & 0xFFFFu);
+            v[2 * i + 1] = (double)bf16_bits_to_float(w[i] >> 16);
+        }
+    }
+};
+
+template <>
+struct Chunk<SPICE_F32> {
+    static constexpr int n = 4;
+    __device__ __forceinline__ static void load(const void* base, size_t elem, double* v) {
+        const float4 q = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + elem);
+        v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+    }
+};
+
+__device__ __forceinline__ double wave_sum_lane0(double v) {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+    return __shfl(v, 0);  // every lane takes lane 0's association order
+}
+
+__device__ __forceinline__ bool is_last_arrival(uint32_t* counter, uint32_t n_expected, int* s_flag) {
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t prev = atomicAdd(counter, 1u);
+        const bool last = (prev == n_expected - 1);
+        if (last) atomicExch(counter, 0u);
+        *s_flag = last ? 1 : 0;
+    }
+    __syncthreads();
+    const bool last = *s_flag != 0;
+    if (last) __threadfence();
+    return last;
+}
+
+// Step 2 for one token: wave-wide softmax over N logits, K rounds of argmax.
+__device__ void topk_one_token(const RouteArgs& a, int t, int lane) {
+    const int N = a.N, K = a.K;
+    constexpr int kJ = SPICE_MAX_EXPERTS / 64;
+    double z[kJ];
+    bool taken[kJ];
+    double m = -DBL_MAX;
+#pragma unroll
+    for (int j = 0; j < kJ; ++j) {
+        const int e = lane + 64 * j;
+        z[j] = (e < N) ? a.logits_ws[(size_t)t * N + e] : -DBL_MAX;
+        taken[j] = (e >= N);
+        if (e < N) m = fmax(m, z[j]);
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) m = fmax(m, __shfl_xor(m, o));
+    double part = 0.0;
+#pragma unroll
+    for (int j = 0; j < kJ; ++j)
+        if (lane + 64 * j < N) part += exp(z[j] - m);
+    const double denom = wave_sum_lane0(part);
+
+    int my_e = -1;
+    double my_z = 0.0;
+    for (int k = 0; k < K; ++k) {
+        double bv = -DBL_MAX;
+        int bi = INT_MAX;
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            const int e = lane + 64 * j;
+            if (!taken[j] && (bi == INT_MAX || z[j] > bv)) { bv = z[j]; bi = e; }
+        }
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) {
+            const double ov = __shfl_xor(bv, o);
+            const int oi = __shfl_xor(bi, o);
+            if (oi != INT_MAX && (bi == INT_MAX || ov > bv || (ov == bv && oi < bi))) { bv = ov; bi = oi; }
+        }
+        if (bi != INT_MAX && (bi & 63) == lane) taken[bi >> 6] = true;
+        if (lane == k) { my_e = bi; my_z = bv; }
+    }
+
+    double g = 0.0;
+    if (lane < K) g = exp(my_z - m) / denom;
+    if (a.norm_topk) g = g / wave_sum_lane0(lane < K ? g : 0.0);
+    const double gsum = (a.conf_mode == SPICE_CONF_GATE_RENORM) ? wave_sum_lane0(lane < K ? g : 0.0) : 1.0;
+    if (lane < K) {
+        const size_t s = (size_t)t * K + lane;
+        float conf;
+        if (a.conf_mode == SPICE_CONF_INPUT) conf = a.conf[s];
+        else if (a.conf_mode == SPICE_CONF_GATE) conf = (float)g;
+        else conf = (float)(g / gsum);
+        int32_t slot = -1;
+        if (my_e >= 0 && my_e < N) slot = a.resident_slot[my_e];
+        if (slot < -1 || slot >= a.C) {
+            atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_SLOT);
+            slot = -1;
+        }
+        uint8_t cls;
+        if (slot >= 0) cls = SPICE_CLASS_HIT;
+        else if (conf < a.tau) cls = SPICE_CLASS_LORE;
+        else cls = SPICE_CLASS_EXACT;
+        a.topk_idx[s] = my_e;
+        a.topk_w[s] = (float)g;
+        a.slot_class[s] = cls;
+    }
+}
+
+// Bucket key of slot s, or -1 (flagged) for a value no gating step can produce.
+__device__ __forceinline__ int slot_key(const RouteArgs& a, int s) {
+    const int c = a.slot_class[s], e = a.topk_idx[s];
+    if (c > SPICE_CLASS_EXACT || e < 0 || e >= a.N) {
+        atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+        return -1;
+    }
+    return c * a.N + e;
+}
+
+// Step 3: stable counting sort of the T*K slots by key = class*N + expert.
+__device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_wsum) {
+    const int N = a.N, S = a.T * a.K, NK = 3 * N;
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    for (int i = tid; i < kWaves * NK; i += kThreads) { s_base[i] = 0; s_run[i] = 0; }
+    __syncthreads();
+    const int per = (S + kWaves - 1) / kWaves;
+    const int lo = min(S, w * per), hi = min(S, lo + per);
+    for (int s = lo + lane; s < hi; s += 64) {
+        const int key = slot_key(a, s);
+        if (key >= 0) atomicAdd(&s_base[w * NK + key], 1);
+    }
+    __syncthreads();
+
+    // Block-wide exclusive scan over keys; thread `tid` owns keys 3*tid .. 3*tid+2.
+    int tot = 0;
+    int cnt[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+        const int key = 3 * tid + q;
+        int v = 0;
+        if (key < NK)
+            for (int ww = 0; ww < kWaves; ++ww) v += s_base[ww * NK + key];
+        cnt[q] = v;
+        tot += v;
+    }
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int up = __shfl_up(incl, o);
+        if (lane >= o) incl += up;
+    }
+    if (lane == 63) s_wsum[w] = incl;
+    __syncthreads();
+    int run = incl - tot;
+    for (int ww = 0; ww < w; ++ww) run += s_wsum[ww];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+        const int key = 3 * tid + q;
+        if (key < NK) {
+            const int c = key / N, e = key - c * N;
+            a.offsets[c * (N + 1) + e] = run;
+            int acc = run;
+            for (int ww = 0; ww < kWaves; ++ww) {
+                const int h = s_base[ww * NK + key];
+                s_base[ww * NK + key] = acc;
+                acc += h;
+            }
+            if (e == N - 1) a.offsets[c * (N + 1) + N] = acc;
+            run += cnt[q];
+        }
+    }
+    __syncthreads();
+
+    const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int base = lo; base < hi; base += 64) {
+        const int s = base + lane;
+        const int key = (s < hi) ? slot_key(a, s) : -1;
+        const bool valid = key >= 0;
+        unsigned long long match = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 10; ++b) {
+            const bool bit = (key >> b) & 1;
+            const unsigned long long bb = __ballot(valid && bit);
+            match &= bit ? bb : ~bb;
+        }
+        if (valid) {
+            const int rank = __popcll(match & lt_mask);
+            const int pos = s_base[w * NK + key] + s_run[w * NK + key] + rank;
+            if (pos >= 0 && pos < S) {
+                a.perm[pos] = s;
+                a.inv_perm[s] = pos;
+            } else {
+                atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+            }
+            if ((match >> lane) == 1ull) s_run[w * NK + key] += __popcll(match);
+        }
+    }
+}
+
+template <int DT>
+__global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a) {
+    __shared__ int s_base[kWaves * kMaxKeys];
+    __shared__ int s_run[kWaves * kMaxKeys];
+    __shared__ int s_wsum[kWaves];
+    __shared__ int s_flag;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int t0 = blockIdx.y * kRouteTok;
+    const int nt = min(kRouteTok, a.T - t0);
+    constexpr int V = Chunk<DT>::n;
+    const int nchunk = a.d / V;
+
+    // 1. logits for (t0 .. t0+nt) x (2 experts of this wave)
+    for (int pe = 0; pe < 2; ++pe) {
+        const int e = blockIdx.x * kRouteExp + w * 2 + pe;
+        if (e >= a.N) break;
+        double acc[kRouteTok];
+#pragma unroll
+        for (int i = 0; i < kRouteTok; ++i) acc[i] = 0.0;
+        for (int c = lane; c < nchunk; c += 64) {
+            double wv[V];
+            Chunk<DT>::load(a.wg, (size_t)e * a.d + (size_t)c * V, wv);
+#pragma unroll
+            for (int i = 0; i < kRouteTok; ++i) {
+                if (i < nt) {
+                    double xv[V];
+                    Chunk<DT>::load(a.x, (size_t)(t0 + i) * a.d + (size_t)c * V, xv);
+#pragma unroll
+                    for (int j = 0; j < V; ++j) acc[i] += xv[j] * wv[j];
+                }
+            }
+        }
+        const double b = a.bias ? (double)a.bias[e] : 0.0;
+#pragma unroll
+        for (int i = 0; i < kRouteTok; ++i) {
+            if (i < nt) {
+                const double zi = wave_sum_lane0(acc[i]) + b;
+                if (lane == 0) {
+                    a.logits_ws[(size_t)(t0 + i) * a.N + e] = zi;
+                    if (a.logits_out) a.logits_out[(size_t)(t0 + i) * a.N + e] = zi;
+                }
+            }
+        }
+    }
+
+    // 2. the last expert group of this token tile runs the gating
+    if (!is_last_arrival(&a.ctrl[kWordTileCounters + blockIdx.y], gridDim.x, &s_flag)) return;
+    for (int i = w; i < nt; i += kWaves) topk_one_token(a, t0 + i, lane);
+
+    // 3. the last token tile buckets every slot
+    if (!is_last_arrival(&a.ctrl[kWordRouteDone], gridDim.y, &s_flag)) return;
+    bucket_all(a, s_base, s_run, s_wsum);
+}
+
+}  // namespace
+
+hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
+    dim3 grid((a.N + kRouteExp - 1) / kRouteExp, (a.T + kRouteTok - 1) / kRouteTok);
+    if (a.dtype == SPICE_BF16)
+        hipLaunchKernelGGL(route_bucket_kernel<SPICE_BF16>, grid, dim3(kThreads), 0, s, a);
+    else
+        hipLaunchKernelGGL(route_bucket_kernel<SPICE_F32>, grid, dim3(kThreads), 0, s, a);
+    return hipGetLastError();
+}
+
+}  // namespace spice

@@ -1,0 +1,89 @@
+// Internal declarations shared by the HIP kernels and the C-ABI layer of libspice_moe.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "spice_moe.h"
+
+namespace spice {
+
+// Workspace control region (32-bit words at the start of every workspace).
+constexpr int kWordFlags = 0;          // device flags, SPICE_FLAG_* (atomic OR)
+constexpr int kWordRouteDone = 1;      // route tiles finished (last one buckets)
+constexpr int kWordTileCounters = 64;  // one counter per route token tile
+constexpr int kRouteTok = 8;           // tokens per route block
+constexpr int kRouteExp = 8;           // experts per route block (2 per wave)
+static_assert((kWordTileCounters + SPICE_MAX_TOKENS / kRouteTok) * 4 <= SPICE_WS_CONTROL_BYTES,
+              "control region too small");
+
+// Byte offsets of the workspace regions for one (cfg, T).
+struct WsLayout {
+    size_t logits;  // fp64 [T][N]
+    size_t h;       // SwiGLU intermediate of routed slots [T*K][I] (dtype)
+    size_t hs;      // shared-block intermediate [T][I_s] (dtype)
+    size_t u;       // LoRE A x, fp32 [T*K][r]
+    size_t total;
+};
+WsLayout ws_layout(const spice_moe_cfg_t& c, int32_t T);
+
+// Which expert groups a grouped-FFN launch covers.
+enum : int { kDoHit = 1, kDoShared = 2, kDoLore = 4 };
+
+struct RouteArgs {
+    int32_t T, d, N, K, C, dtype, norm_topk, conf_mode;
+    float tau;
+    const void* x;
+    const void* wg;
+    const float* bias;
+    const int32_t* resident_slot;
+    const float* conf;
+    double* logits_out;   // caller's, nullable
+    double* logits_ws;    // workspace copy read by the top-K step
+    int32_t* topk_idx;
+    float* topk_w;
+    uint8_t* slot_class;
+    int32_t* offsets;
+    int32_t* perm;
+    int32_t* inv_perm;
+    uint32_t* ctrl;       // workspace control words
+};
+
+struct FfnArgs {
+    int32_t T, d, N, K, C, I, Is, r, dtype, groups;
+    const void* x;
+    const int32_t* perm;
+    const int32_t* offsets;
+    const int32_t* resident_slot;
+    const void* w13_pool;
+    const void* w2_pool;
+    const void* w13s;
+    const void* w2s;
+    const void* lore_A;
+    const void* lore_B;
+    float* y_slots;
+    float* y_shared;
+    void* h;        // workspace [T*K][I]
+    void* hs;       // workspace [T][I_s]
+    float* u;       // workspace [T*K][r]
+    uint32_t* ctrl;
+};
+
+struct CombineArgs {
+    int32_t T, d, K, dtype;
+    const float* topk_w;
+    const uint8_t* slot_class;
+    const int32_t* inv_perm;
+    const float* y_slots;
+    const float* y_shared;
+    const float* resid;
+    void* out;
+};
+
+hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
+hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+hipError_t launch_fill_u32(uint32_t* p, size_t words, uint32_t value, hipStream_t s);
+
+}  // namespace spice

@@ -1,0 +1,229 @@
+"""Driver of one MoE layer call through the C ABI (memory and streams only).
+
+``HostLayer`` holds the seeded weights of one layer in NumPy; ``DeviceLayer``
+puts the resident experts into an HBM slot pool, plus the router, the shared
+block and every expert's LoRE factors, and keeps the non-resident experts on
+the host for the exact CPU path.  ``LayerRun`` owns the per-call buffers and
+runs the path in the order the paper describes (Sec. 4.3):
+
+    stream s   : route+bucket -> grouped FFN (+LoRE) ............ wait(e_h2d) -> combine
+    copy stream:        wait(route) -> D2H x, idx, gates, classes    H2D resid -> e_h2d
+    host       :                       sync -> exact residual (CPU threads)
+
+Every arithmetic step runs inside libspice_moe (HIP kernels or its host path).
+"""
+from __future__ import annotations
+
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+import torch
+
+from . import spice, synth
+from .workloads import DTYPE_BF16, Workload
+
+
+def torch_dtype(dtype: int) -> torch.dtype:
+    return torch.bfloat16 if dtype == DTYPE_BF16 else torch.float32
+
+
+def to_tensor(a: np.ndarray, dtype: int, device=None, pin: bool = False) -> torch.Tensor:
+    """Storage array (float32 or bf16 bits) -> tensor of the storage dtype."""
+    if dtype == DTYPE_BF16:
+        t = torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16)
+    else:
+        t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32))
+    if pin:
+        return t.pin_memory()
+    return t.to(device) if device is not None else t
+
+
+class HostLayer:
+    """Seeded weights of one layer (storage arrays), drawn lazily per expert."""
+
+    def __init__(self, wl: Workload, layer: int = 0, resident: Optional[Sequence[int]] = None):
+        self.wl, self.layer, self.shape = wl, layer, wl.shape
+        self.resident = list(synth.resident_experts(wl, layer) if resident is None else resident)
+        self.wg = synth.gen_router(wl, layer)
+        self.bias = synth.gen_bias(wl, layer)
+        self.w13s, self.w2s = synth.gen_shared(wl, layer)
+        self._experts: Dict[int, tuple] = {}
+        self._lore: Dict[int, tuple] = {}
+
+    def expert(self, e: int):
+        if e not in self._experts:
+            self._experts[e] = synth.gen_expert(self.wl, self.layer, e)
+        return self._experts[e]
+
+    def lore(self, e: int):
+        if e not in self._lore:
+            self._lore[e] = synth.gen_lore(self.wl, self.layer, e)
+        return self._lore[e]
+
+    def resident_mask(self) -> np.ndarray:
+        m = np.zeros(self.shape.n_experts, np.int32)
+        m[self.resident] = 1
+        return m
+
+    def tables(self, experts: Sequence[int], lore_experts: Sequence[int]):
+        """Per-expert weight tables of length N (None where not requested)."""
+        N = self.shape.n_experts
+        w13: List = [None] * N; w2: List = [None] * N; la: List = [None] * N; lb: List = [None] * N
+        for e in experts:
+            w13[e], w2[e] = self.expert(e)
+        for e in lore_experts:
+            la[e], lb[e] = self.lore(e)
+        return w13, w2, la, lb
+
+
+class DeviceLayer:
+    """Device copy of a layer: pool of resident experts, router, shared block, LoRE factors."""
+
+    def __init__(self, host: HostLayer, n_slots: Optional[int] = None, device: str = "cuda",
+                 host_exact: bool = True):
+        s, dt = host.shape, host.shape.dtype
+        self.host, self.shape = host, s
+        self.C = len(host.resident) if n_slots is None else n_slots
+        td = torch_dtype(dt)
+        self.wg = to_tensor(host.wg, dt, device)
+        self.bias = None if host.bias is None else torch.from_numpy(host.bias).to(device)
+        self.w13s = to_tensor(host.w13s, dt, device)
+        self.w2s = to_tensor(host.w2s, dt, device)
+        slot = np.full(s.n_experts, -1, np.int32)
+        self.w13_pool = torch.empty((max(self.C, 1), 2 * s.inter, s.d), dtype=td, device=device)
+        self.w2_pool = torch.empty((max(self.C, 1), s.d, s.inter), dtype=td, device=device)
+        for i, e in enumerate(host.resident):
+            w13, w2 = host.expert(e)
+            self.w13_pool[i].copy_(to_tensor(w13, dt))
+            self.w2_pool[i].copy_(to_tensor(w2, dt))
+            slot[e] = i
+        self.resident_slot = torch.from_numpy(slot).to(device)
+        r = max(s.lore_rank, 1)
+        self.lore_A = torch.empty((s.n_experts, r, s.d), dtype=td, device=device)
+        self.lore_B = torch.empty((s.n_experts, s.d, r), dtype=td, device=device)
+        if s.lore_rank > 0:
+            for e in range(s.n_experts):
+                A, B = host.lore(e)
+                self.lore_A[e].copy_(to_tensor(A, dt))
+                self.lore_B[e].copy_(to_tensor(B, dt))
+        # host-resident weights of the non-resident experts (the exact CPU path)
+        self.host_w13: List = [None] * s.n_experts
+        self.host_w2: List = [None] * s.n_experts
+        if host_exact:
+            for e in range(s.n_experts):
+                if slot[e] < 0:
+                    self.host_w13[e], self.host_w2[e] = host.expert(e)
+
+    def hbm_bytes(self) -> int:
+        ts = [self.wg, self.w13s, self.w2s, self.w13_pool, self.w2_pool, self.lore_A, self.lore_B]
+        return sum(t.numel() * t.element_size() for t in ts)
+
+
+class LayerRun:
+    """Buffers and streams for layer calls with up to T tokens."""
+
+    def __init__(self, shape, T: int, n_slots: int, tau: float = 0.5, conf_mode: int = 0, norm_topk: int = 0,
+                 device: str = "cuda", keep_logits: bool = False):
+        self.shape, self.T = shape, T
+        self.cfg = spice.make_cfg(shape, n_slots, tau, conf_mode, norm_topk)
+        s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
+        i32 = dict(dtype=torch.int32, device=device)
+        f32 = dict(dtype=torch.float32, device=device)
+        self.topk_idx = torch.empty((T, K), **i32)
+        self.topk_w = torch.empty((T, K), **f32)
+        self.slot_class = torch.empty((T, K), dtype=torch.uint8, device=device)
+        self.offsets = torch.empty((3, N + 1), **i32)
+        self.perm = torch.empty(T * K, **i32)
+        self.inv_perm = torch.empty(T * K, **i32)
+        self.logits = torch.empty((T, N), dtype=torch.float64, device=device) if keep_logits else None
+        self.y_slots = torch.zeros((T * K, d), **f32)
+        self.y_shared = torch.zeros((T, d), **f32)
+        self.resid = torch.zeros((T, d), **f32)
+        self.out = torch.empty((T, d), dtype=torch_dtype(s.dtype), device=device)
+        self.ws_bytes = spice.spice_workspace_bytes(self.cfg, T)
+        if self.ws_bytes == 0:
+            raise ValueError(f"invalid configuration for the library: {spice.last_error()}")
+        self.ws = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
+        # pinned staging for the exact CPU path
+        self.x_host = torch.empty((T, d), dtype=torch_dtype(s.dtype)).pin_memory()
+        self.idx_host = torch.empty((T, K), dtype=torch.int32).pin_memory()
+        self.w_host = torch.empty((T, K), dtype=torch.float32).pin_memory()
+        self.cls_host = torch.empty((T, K), dtype=torch.uint8).pin_memory()
+        self.resid_host = torch.zeros((T, d), dtype=torch.float32).pin_memory()
+        self.copy_stream = torch.cuda.Stream(device=device)
+        self.e_route = torch.cuda.Event()
+        self.e_d2h = torch.cuda.Event()
+        self.e_h2d = torch.cuda.Event()
+
+    # -- the steps, each one C-ABI call ------------------------------------------------
+    def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None):
+        T = self.T if T is None else T
+        spice.moe_route_bucket(self.cfg, T, x, L.wg, L.bias, L.resident_slot, conf, self.logits, self.topk_idx,
+                               self.topk_w, self.slot_class, self.offsets, self.perm, self.inv_perm, self.ws,
+                               self.ws_bytes)
+
+    def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
+        T = self.T if T is None else T
+        spice.moe_expert_ffn_grouped(self.cfg, T, x, self.perm, self.offsets, L.resident_slot, L.w13_pool,
+                                     L.w2_pool, L.w13s, L.w2s, L.lore_A if fuse_lore else None,
+                                     L.lore_B if fuse_lore else None, self.y_slots, self.y_shared, self.ws,
+                                     self.ws_bytes)
+
+    def lore(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None):
+        T = self.T if T is None else T
+        spice.lore_surrogate_apply(self.cfg, T, x, self.perm, self.offsets, L.lore_A, L.lore_B, self.y_slots,
+                                   self.ws, self.ws_bytes)
+
+    def combine(self, resid: Optional[torch.Tensor], T: Optional[int] = None):
+        T = self.T if T is None else T
+        spice.moe_combine(self.cfg, T, self.topk_w, self.slot_class, self.inv_perm, self.y_slots, self.y_shared,
+                          resid, self.out)
+
+    def stage_to_host(self, x: torch.Tensor, T: int):
+        """On the copy stream, after routing: D2H of what the exact CPU path reads."""
+        main = torch.cuda.current_stream()
+        self.e_route.record(main)
+        with torch.cuda.stream(self.copy_stream):
+            self.copy_stream.wait_event(self.e_route)
+            self.x_host[:T].copy_(x[:T], non_blocking=True)
+            self.idx_host[:T].copy_(self.topk_idx[:T], non_blocking=True)
+            self.w_host[:T].copy_(self.topk_w[:T], non_blocking=True)
+            self.cls_host[:T].copy_(self.slot_class[:T], non_blocking=True)
+            self.e_d2h.record(self.copy_stream)
+
+    def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0):
+        """Wait for the staged routing results, run the CPU residual, H2D it on the copy stream."""
+        self.e_d2h.synchronize()
+        spice.moe_exact_residual_host(self.cfg, T, self.x_host, self.idx_host, self.w_host, self.cls_host,
+                                      L.host_w13, L.host_w2, self.resid_host, n_threads)
+        with torch.cuda.stream(self.copy_stream):
+            self.resid[:T].copy_(self.resid_host[:T], non_blocking=True)
+            self.e_h2d.record(self.copy_stream)
+        torch.cuda.current_stream().wait_event(self.e_h2d)
+
+    def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
+                exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None):
+        """One layer call: route, FFN + LoRE on the GPU overlapped with the exact CPU residual, combine."""
+        T = self.T if T is None else T
+        ev = events or {}
+        if "start" in ev:
+            ev["start"].record()
+        self.route(L, x, conf, T)
+        if "routed" in ev:
+            ev["routed"].record()
+        if exact:
+            self.stage_to_host(x, T)
+        self.experts(L, x, T, fuse_lore=True)
+        if "experts" in ev:
+            ev["experts"].record()
+        if exact:
+            self.exact_host(L, T, n_threads)
+        if "resid" in ev:
+            ev["resid"].record()
+        self.combine(self.resid if exact else None, T)
+        if "end" in ev:
+            ev["end"].record()
+        return self.out[:T]
+
+    def flags(self, clear: bool = True) -> int:
+        return spice.spice_workspace_flags(self.ws, self.ws_bytes, clear)

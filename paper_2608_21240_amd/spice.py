@@ -1,0 +1,172 @@
+"""ctypes binding of libspice_moe.so: the C-ABI entry points under the same names.
+
+Argument marshalling only.  Buffers may be passed as torch tensors (their
+data_ptr() is used), NumPy arrays (host buffers), raw integer addresses or
+None.  Streams default to torch's current HIP stream.  A non-zero status
+raises SpiceError with the library's message.  There is no fallback: if the
+library is missing, loading raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libspice_moe.so")
+
+SPICE_OK, SPICE_ERR_INVALID, SPICE_ERR_UNSUPPORTED, SPICE_ERR_HIP, SPICE_ERR_WORKSPACE, SPICE_ERR_INTERNAL = (
+    0, -1, -2, -3, -4, -5)
+SPICE_F32, SPICE_BF16 = 0, 1
+SPICE_CONF_INPUT, SPICE_CONF_GATE, SPICE_CONF_GATE_RENORM = 0, 1, 2
+SPICE_CLASS_HIT, SPICE_CLASS_LORE, SPICE_CLASS_EXACT = 0, 1, 2
+SPICE_MAX_EXPERTS, SPICE_MAX_TOKENS, SPICE_MAX_LORE_RANK = 256, 65536, 256
+SPICE_WS_CONTROL_BYTES = 65536
+SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
+
+# Every function the header declares (checked against include/spice_moe.h by the tests).
+EXPORTS = (
+    "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
+    "moe_route_bucket", "moe_expert_ffn_grouped", "lore_surrogate_apply", "moe_combine",
+    "moe_exact_residual_host", "spice_status_string", "spice_last_error",
+)
+
+
+class SpiceError(RuntimeError):
+    def __init__(self, fn: str, status: int, msg: str):
+        super().__init__(f"{fn}: status {status}: {msg}")
+        self.status = status
+
+
+class spice_moe_cfg_t(ctypes.Structure):
+    _fields_ = [("d", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
+                ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
+                ("n_slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32),
+                ("conf_mode", ctypes.c_int32), ("tau", ctypes.c_float)]
+
+
+def make_cfg(shape, n_slots: int, tau: float = 0.5, conf_mode: int = SPICE_CONF_INPUT,
+             norm_topk: int = 0) -> spice_moe_cfg_t:
+    return spice_moe_cfg_t(shape.d, shape.n_experts, shape.top_k, shape.inter, shape.shared_inter,
+                           shape.lore_rank, n_slots, shape.dtype, norm_topk, conf_mode, tau)
+
+
+_lib: Optional[ctypes.CDLL] = None
+_P, _I, _Z = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run `python -m paper_2608_21240_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        C = ctypes.POINTER(spice_moe_cfg_t)
+        sig = {
+            "spice_workspace_bytes": (_Z, [C, _I]),
+            "spice_workspace_init": (_I, [_P, _Z, _P]),
+            "spice_workspace_flags": (_I, [_P, _Z, ctypes.POINTER(ctypes.c_uint32), _I, _P]),
+            "moe_route_bucket": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+            "moe_expert_ffn_grouped": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+            "lore_surrogate_apply": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+            "moe_combine": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+            "moe_exact_residual_host": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I]),
+            "spice_status_string": (ctypes.c_char_p, [_I]),
+            "spice_last_error": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _p(a):
+    """Address of a buffer argument."""
+    if a is None:
+        return None
+    if isinstance(a, int):
+        return a
+    if hasattr(a, "data_ptr"):
+        return a.data_ptr()
+    if hasattr(a, "ctypes"):
+        return a.ctypes.data
+    if isinstance(a, ctypes.Array):
+        return ctypes.addressof(a)
+    raise TypeError(f"cannot pass {type(a).__name__} as a buffer")
+
+
+def _stream(s):
+    if s is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def _check(fn: str, st: int) -> None:
+    if st != SPICE_OK:
+        raise SpiceError(fn, st, lib().spice_last_error().decode())
+
+
+def last_error() -> str:
+    return lib().spice_last_error().decode()
+
+
+def spice_status_string(status: int) -> str:
+    return lib().spice_status_string(status).decode()
+
+
+def spice_workspace_bytes(cfg: spice_moe_cfg_t, T: int) -> int:
+    return lib().spice_workspace_bytes(ctypes.byref(cfg), T)
+
+
+def spice_workspace_init(ws, ws_bytes: int, stream=None) -> None:
+    _check("spice_workspace_init", lib().spice_workspace_init(_p(ws), ws_bytes, _stream(stream)))
+
+
+def spice_workspace_flags(ws, ws_bytes: int, clear: bool = False, stream=None) -> int:
+    f = ctypes.c_uint32(0)
+    _check("spice_workspace_flags",
+           lib().spice_workspace_flags(_p(ws), ws_bytes, ctypes.byref(f), int(clear), _stream(stream)))
+    return f.value
+
+
+def moe_route_bucket(cfg, T, x, w_gate, logit_bias, resident_slot, conf, logits, topk_idx, topk_w, slot_class,
+                     offsets, perm, inv_perm, ws, ws_bytes, stream=None) -> None:
+    _check("moe_route_bucket", lib().moe_route_bucket(
+        ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(logits),
+        _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm), _p(ws), ws_bytes,
+        _stream(stream)))
+
+
+def moe_expert_ffn_grouped(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared,
+                           lore_A, lore_B, y_slots, y_shared, ws, ws_bytes, stream=None) -> None:
+    _check("moe_expert_ffn_grouped", lib().moe_expert_ffn_grouped(
+        ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(resident_slot), _p(w13_pool), _p(w2_pool),
+        _p(w13_shared), _p(w2_shared), _p(lore_A), _p(lore_B), _p(y_slots), _p(y_shared), _p(ws), ws_bytes,
+        _stream(stream)))
+
+
+def lore_surrogate_apply(cfg, T, x, perm, offsets, lore_A, lore_B, y_slots, ws, ws_bytes, stream=None) -> None:
+    _check("lore_surrogate_apply", lib().lore_surrogate_apply(
+        ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(lore_A), _p(lore_B), _p(y_slots), _p(ws),
+        ws_bytes, _stream(stream)))
+
+
+def moe_combine(cfg, T, topk_w, slot_class, inv_perm, y_slots, y_shared, resid, out, stream=None) -> None:
+    _check("moe_combine", lib().moe_combine(
+        ctypes.byref(cfg), T, _p(topk_w), _p(slot_class), _p(inv_perm), _p(y_slots), _p(y_shared), _p(resid),
+        _p(out), _stream(stream)))
+
+
+def moe_exact_residual_host(cfg, T, x_host, topk_idx_host, topk_w_host, slot_class_host,
+                            w13_host: Sequence, w2_host: Sequence, resid_host, n_threads: int = 0) -> None:
+    """w13_host / w2_host: length-N sequences of host buffers (or None)."""
+    t13 = (ctypes.c_void_p * len(w13_host))(*[_p(w) for w in w13_host])
+    t2 = (ctypes.c_void_p * len(w2_host))(*[_p(w) for w in w2_host])
+    _check("moe_exact_residual_host", lib().moe_exact_residual_host(
+        ctypes.byref(cfg), T, _p(x_host), _p(topk_idx_host), _p(topk_w_host), _p(slot_class_host), t13, t2,
+        _p(resid_host), n_threads))

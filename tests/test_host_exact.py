@@ -1,0 +1,93 @@
+"""The library's host-side exact residual (Sec. 4.3, M_cpu) against the oracle, on the CPU."""
+import numpy as np
+import pytest
+
+from paper_2608_21240_amd import spice, synth, workloads as W
+
+HIT, LORE, EXACT = 0, 1, 2
+
+
+def rel_err(out, ref):
+    """Per-token max |out - ref| / max |ref|, the tolerance metric of the parity tests."""
+    num = np.abs(out - ref).max(axis=1)
+    den = np.maximum(np.abs(ref).max(axis=1), 1e-30)
+    return num / den
+
+
+def setup(orc, shape, T, seed, exact_frac=0.6, resident_frac=0.3):
+    wl = W.Workload("t", shape, tokens=T, resident=0, skew=False, seed=seed)
+    r = np.random.default_rng(seed)
+    N = shape.n_experts
+    resident = np.zeros(N, np.int32)
+    resident[r.permutation(N)[: int(resident_frac * N)]] = 1
+    x = synth.gen_x(wl)
+    wg = synth.gen_router(wl)
+    conf = np.where(r.random((T, shape.top_k)) < exact_frac, 0.9, 0.1).astype(np.float32)
+    cfg = orc.make_cfg(shape)
+    rt = orc.route(cfg, x, wg, None, resident, conf)
+    experts = sorted(set(rt["idx"][rt["cls"] == EXACT].tolist()))
+    w13 = [None] * N
+    w2 = [None] * N
+    for e in experts:
+        w13[e], w2[e] = synth.gen_expert(wl, 0, e)
+    return wl, cfg, x, rt, w13, w2
+
+
+@pytest.mark.parametrize("shape,T,seed", [
+    (W.TINY, 4, 0),
+    (W.small_shape(dtype=W.DTYPE_F32), 9, 1),
+    (W.small_shape(), 13, 2),
+    (W.MoEShape(2048, 64, 6, 1408, 2816, 32, W.DTYPE_BF16), 3, 3),
+])
+def test_exact_residual_matches_oracle(orc, shape, T, seed):
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, T, seed)
+    ref = orc.exact_residual(cfg, x, rt["idx"], rt["g"], rt["cls"], w13, w2)
+    c = spice.make_cfg(shape, n_slots=0)
+    out = np.full((T, shape.d), np.nan, np.float32)
+    gw = rt["g"].astype(np.float32)
+    spice.moe_exact_residual_host(c, T, x, rt["idx"], gw, rt["cls"], w13, w2, out, n_threads=4)
+    has = (rt["cls"] == EXACT).any(axis=1)
+    assert has.any()
+    assert (out[~has] == 0).all()
+    tol = 1e-4  # fp32 arithmetic on exact inputs, for fp32 and bf16 storage alike
+    assert rel_err(out[has], ref[has]).max() < tol
+
+
+def test_result_is_independent_of_thread_count(orc):
+    shape = W.small_shape()
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, 21, 5)
+    c = spice.make_cfg(shape, n_slots=0)
+    outs = []
+    for nt in (1, 2, 3, 8):
+        out = np.empty((21, shape.d), np.float32)
+        spice.moe_exact_residual_host(c, 21, x, rt["idx"], rt["g"].astype(np.float32), rt["cls"], w13, w2, out,
+                                      n_threads=nt)
+        outs.append(out)
+    for o in outs[1:]:
+        assert np.array_equal(o, outs[0])
+
+
+def test_degenerate_inputs(orc):
+    shape = W.small_shape()
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, 6, 6)
+    c = spice.make_cfg(shape, n_slots=0)
+    out = np.full((6, shape.d), 7.0, np.float32)
+    # T == 0: nothing is touched
+    spice.moe_exact_residual_host(c, 0, x, rt["idx"], rt["g"].astype(np.float32), rt["cls"], w13, w2, out)
+    assert (out == 7.0).all()
+    # no exact slot: zero residual, no weights needed
+    cls = np.where(rt["cls"] == EXACT, LORE, rt["cls"]).astype(np.uint8)
+    spice.moe_exact_residual_host(c, 6, x, rt["idx"], rt["g"].astype(np.float32), cls, [None] * 16, [None] * 16,
+                                  out)
+    assert (out == 0).all()
+    # an exact-miss expert without weights, a bad class, a bad expert id
+    with pytest.raises(spice.SpiceError) as e:
+        spice.moe_exact_residual_host(c, 6, x, rt["idx"], rt["g"].astype(np.float32), rt["cls"], [None] * 16,
+                                      [None] * 16, out)
+    assert e.value.status == spice.SPICE_ERR_INVALID
+    bad = rt["cls"].copy(); bad[0, 0] = 3
+    with pytest.raises(spice.SpiceError):
+        spice.moe_exact_residual_host(c, 6, x, rt["idx"], rt["g"].astype(np.float32), bad, w13, w2, out)
+    badi = rt["idx"].copy(); badi[rt["cls"] == EXACT] = 99
+    with pytest.raises(spice.SpiceError):
+        spice.moe_exact_residual_host(c, 6, x, badi, rt["g"].astype(np.float32), rt["cls"], w13, w2, out)
