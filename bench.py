@@ -1,0 +1,243 @@
+"""MoE-layer decode benchmark: SPICE's per-layer forward under a partial expert cache.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+
+Workload: a DeepSeek-V2-Lite-shaped MoE layer (hidden 2048, 64 routed experts of
+SwiGLU intermediate 1408, shared block 2816, top-6 softmax gating, LoRE rank 32),
+bf16 weights/activations with fp32 accumulation, 32 experts resident (Zipf(1.1)
+popularity), per-slot confidence U(0,1) with tau = 0.5; decode batch 32 is the
+headline, batches 1 and 8 are reported alongside.  Weights and inputs are
+seeded synthetic draws.
+
+One step = one whole layer call on one batch: routing + bucketing, grouped FFN of
+the resident hits + shared block + LoRE corrections on the GPU, the exact-miss
+residual on the host CPU (overlapped with the GPU work), and the combine.
+Steps rotate over several independent layer instances so that the weights
+(about 0.6 GB per instance) stream from HBM and not from the 256 MB MALL.
+
+Prints one JSON line.  ``roofline`` is for the dominant kernel, the grouped FFN
+launch, timed with HIP events on its stream; ``cpu_baseline`` is the plain fp64
+oracle on a bounded sample of the same workload, on one host core.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shaped"
+
+# HBM traffic of one grouped-FFN call (up + down kernels) at the headline batch, from
+# two rocprofv3 --pmc passes over this script (FETCH_SIZE, then WRITE_SIZE; KiB per
+# dispatch) scaled by what the counters read for a plain 1 GiB device copy
+# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Reported only while the kernel source is the
+# one the counters were taken on.
+TRAFFIC_RECORD = {
+    "kernel_source": "paper_2608_21240_amd/csrc/expert_ffn.hip",
+    "source_sha256_16": "bbb39a0f198b7fae",
+    "fetch_kib_per_call": 189670 + 98806,
+    "write_kib_per_call": 463 + 1451,
+    "fetch_factor": 2.0,
+    "write_factor": 1.0,
+    "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
+}
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=60)
+    p.add_argument("--warmup", type=int, default=6)
+    p.add_argument("--instances", type=int, default=4, help="independent layer instances to rotate over")
+    p.add_argument("--batches", default="1,8,32", help="decode batch sizes; the last is the headline")
+    p.add_argument("--threads", type=int, default=0, help="host threads of the exact CPU path (0 = all)")
+    p.add_argument("--cpu-baseline-seconds", type=float, default=12.0)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--calib-copy-mib", type=int, default=0,
+                   help="finish with a plain device copy of this many MiB (a known-size reference for counters)")
+    return p.parse_args()
+
+
+def recorded_traffic():
+    """HBM bytes per grouped-FFN call from the counter record, or None if the kernel changed."""
+    import hashlib
+
+    path = os.path.join(ROOT, TRAFFIC_RECORD["kernel_source"])
+    sha = hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    if sha != TRAFFIC_RECORD["source_sha256_16"]:
+        return None
+    return int(1024 * (TRAFFIC_RECORD["fetch_kib_per_call"] * TRAFFIC_RECORD["fetch_factor"]
+                       + TRAFFIC_RECORD["write_kib_per_call"] * TRAFFIC_RECORD["write_factor"]))
+
+
+def algorithmic_bytes(shape, idx, cls):
+    """Bytes the method must move on the GPU for one layer call, by kernel.
+
+    ffn: distinct HIT experts x expert bytes + shared block + distinct LoRE experts x
+         factor bytes + x read + y rows written (HIT/LoRE slots fp32, shared fp32).
+    route: router weight + x.  combine: y rows + shared + resid read, out written."""
+    T, K = idx.shape
+    d, wb = shape.d, shape.wbytes
+    hit_e = len(set(idx[cls == 0].tolist()))
+    lore_e = len(set(idx[cls == 1].tolist()))
+    n_hit, n_lore = int((cls == 0).sum()), int((cls == 1).sum())
+    x_b = T * d * wb
+    ffn = (hit_e * shape.expert_bytes + shape.shared_bytes + lore_e * shape.lore_bytes + x_b
+           + (n_hit + n_lore) * d * 4 + T * d * 4)
+    route = shape.n_experts * d * wb + x_b
+    combine = (n_hit + n_lore) * d * 4 + 2 * T * d * 4 + T * d * wb
+    return dict(ffn=ffn, route=route, combine=combine, total=ffn + route + combine, hit_experts=hit_e,
+                lore_experts=lore_e, slots=np.bincount(cls.ravel(), minlength=3).tolist(),
+                exact_experts=len(set(idx[cls == 2].tolist())))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the layer path is single-GPU; "
+              "see the sharding notes in DESIGN.md)", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    from paper_2608_21240_amd import layer as LY, synth, workloads as W
+
+    torch.cuda.set_device(0)
+    batches = [int(b) for b in args.batches.split(",")]
+    wl = W.WORKLOADS["dsv2_decode_t32"]
+    shape = wl.shape
+    t_gen = time.time()
+    hosts, devs = [], []
+    for i in range(args.instances):
+        h = LY.HostLayer(wl, layer=i)
+        devs.append(LY.DeviceLayer(h))
+        hosts.append(h)
+    torch.cuda.synchronize()
+    print(f"[bench] {args.instances} layer instances ready in {time.time() - t_gen:.1f}s "
+          f"({devs[0].hbm_bytes() / 1e9:.2f} GB HBM each)", file=sys.stderr, flush=True)
+
+    results = {}
+    for T in batches:
+        run = LY.LayerRun(shape, T, devs[0].C, tau=wl.tau)
+        xs = [LY.to_tensor(synth.gen_x(wl, i, 0, T), shape.dtype, "cuda") for i in range(args.instances)]
+        confs = [torch.from_numpy(synth.gen_conf(wl, i, 0, T)).cuda() for i in range(args.instances)]
+        # per-instance class counts (fixed inputs per instance) from one untimed call
+        per_inst = []
+        for i in range(args.instances):
+            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
+            torch.cuda.synchronize()
+            per_inst.append(algorithmic_bytes(shape, run.idx_host[:T].numpy().copy(),
+                                              run.cls_host[:T].numpy().copy()))
+        for w in range(args.warmup):
+            i = w % args.instances
+            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
+        torch.cuda.synchronize()
+        if run.flags() != 0:
+            raise RuntimeError("device flags raised during warmup")
+
+        names = ("start", "routed", "ffn0", "experts", "resid", "end")
+        evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
+        host_s = 0.0
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for k in range(args.steps):
+            i = k % args.instances
+            h0 = time.perf_counter()
+            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, events=evs[k])
+            host_s += time.perf_counter() - h0
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+
+        ffn_ms = np.array([e["ffn0"].elapsed_time(e["experts"]) for e in evs])
+        route_ms = np.array([e["start"].elapsed_time(e["routed"]) for e in evs])
+        comb_ms = np.array([e["resid"].elapsed_time(e["end"]) for e in evs])
+        wait_ms = np.array([e["experts"].elapsed_time(e["resid"]) for e in evs])
+        inst = [k % args.instances for k in range(args.steps)]
+        ffn_bytes = np.array([per_inst[i]["ffn"] for i in inst], dtype=np.float64)
+        tot_bytes = np.array([per_inst[i]["total"] for i in inst], dtype=np.float64)
+        gpu_ms = route_ms + ffn_ms + comb_ms
+        results[T] = dict(
+            T=T, wall_s=wall, ms_per_step=1e3 * wall / args.steps,
+            tokens_per_s=T * args.steps / wall,
+            gpu_ms_per_step=float(gpu_ms.mean()),
+            gpu_tokens_per_s=float(T / (gpu_ms.mean() * 1e-3)),
+            gpu_GBps=float(tot_bytes.sum() / (gpu_ms.sum() * 1e-3) / 1e9),
+            route_us=float(route_ms.mean() * 1e3), ffn_us=float(ffn_ms.mean() * 1e3),
+            combine_us=float(comb_ms.mean() * 1e3), wait_for_host_us=float(wait_ms.mean() * 1e3),
+            ffn_GBps=float(ffn_bytes.sum() / (ffn_ms.sum() * 1e-3) / 1e9),
+            ffn_bytes_per_launch=float(ffn_bytes.mean()),
+            classes=per_inst[0]["slots"], hit_experts=[p["hit_experts"] for p in per_inst],
+            lore_experts=[p["lore_experts"] for p in per_inst], exact_experts=[p["exact_experts"] for p in per_inst],
+        )
+        print(f"[bench] T={T}: {json.dumps(results[T])}", file=sys.stderr, flush=True)
+        del run
+
+    head = results[batches[-1]]
+    line = {
+        "metric": METRIC, "value": round(head["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(head["ms_per_step"], 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init DSV2-Lite-shaped layers, Zipf(1.1) residency, conf~U(0,1))",
+        "config": {"workload": f"dsv2_lite_moe_layer_decode_T{head['T']}", "hidden": shape.d,
+                   "experts": shape.n_experts, "top_k": shape.top_k, "inter": shape.inter,
+                   "shared_inter": shape.shared_inter, "lore_rank": shape.lore_rank, "resident": wl.resident,
+                   "tau": wl.tau, "tokens": head["T"], "layer_instances": args.instances,
+                   "host_threads": args.threads or os.cpu_count()},
+        "roofline": {"bound": "hbm", "kernel": "grouped expert FFN call: ffn_up_kernel + ffn_down_kernel "
+                                               "(moe_expert_ffn_grouped with LoRE fused)",
+                     "achieved": round(head["ffn_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(head["ffn_GBps"] / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(),
+                     "bytes_per_launch": int(head["ffn_bytes_per_launch"]), "avg_launch_us": round(head["ffn_us"], 2)},
+        "gpu_path": {"tokens_per_s": round(head["gpu_tokens_per_s"], 1), "ms_per_step": round(head["gpu_ms_per_step"], 4),
+                     "GBps": round(head["gpu_GBps"], 1), "frac_hbm_peak": round(head["gpu_GBps"] / HBM_PEAK_GBS, 4),
+                     "route_us": round(head["route_us"], 2), "ffn_us": round(head["ffn_us"], 2),
+                     "combine_us": round(head["combine_us"], 2)},
+        "by_batch": {str(T): {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()}
+                     for T, r in results.items()},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl.with_(tokens=head["T"]), hosts[0], args.cpu_baseline_seconds)
+    if args.calib_copy_mib > 0:
+        a = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
+        torch.empty_like(a).copy_(a)
+        torch.cuda.synchronize()
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(wl, host, budget_s):
+    """The oracle (fp64, one thread) on whole layer calls of the same workload,
+    batch after batch, until about budget_s seconds of CPU work are done."""
+    import oracle as orc
+    from paper_2608_21240_amd import synth
+
+    s = wl.shape
+    cfg = orc.make_cfg(s, tau=wl.tau)
+    w13, w2, la, lb = host.tables(range(s.n_experts), range(s.n_experts))
+    tokens = 0
+    steps = 0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        x = synth.gen_x(wl, 0, 1000 + steps, wl.tokens)
+        conf = synth.gen_conf(wl, 0, 1000 + steps, wl.tokens)
+        r = orc.route(cfg, x, host.wg, host.bias, host.resident_mask(), conf)
+        for t in range(wl.tokens):
+            orc.token_output(cfg, x[t], r["idx"][t], r["g"][t], r["cls"][t], w13, w2, host.w13s, host.w2s, la, lb)
+            tokens += 1
+            if time.perf_counter() - t0 >= budget_s:
+                break
+        steps += 1
+    el = time.perf_counter() - t0
+    return {"value": round(tokens / el, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{tokens} tokens ({steps} batch(es) of {wl.tokens}) of one DSV2-Lite layer: routing for the "
+                      f"whole batch + full fp64 layer output per token, {el:.1f}s"}
+
+
+if __name__ == "__main__":
+    main()

@@ -67,7 +67,7 @@ enum { SPICE_CLASS_HIT = 0, SPICE_CLASS_LORE = 1, SPICE_CLASS_EXACT = 2 };
 /* The first SPICE_WS_CONTROL_BYTES of a workspace hold counters and flags.
  * They must be zero before the workspace is first used (spice_workspace_init,
  * or any zero fill); every completed call leaves the counters zero again. */
-#define SPICE_WS_CONTROL_BYTES 65536
+#define SPICE_WS_CONTROL_BYTES 131072
 
 /* Device-side flags (bit mask) raised in the workspace by a kernel that met bad data. */
 #define SPICE_FLAG_BAD_SLOT 1u   /* resident_slot[e] outside [-1, n_slots) */

@@ -1,10 +1,12 @@
 // Router logits, softmax top-K gating, per-slot classification and (class, expert)
 // bucketing in one launch (Eq. 1; Sec. 2.1, 4.2, 4.3).
 //
-// Grid: (ceil(N/8) expert groups) x (ceil(T/8) token tiles), 256 threads.
-//   1. every block: fp64 logits of 8 tokens x 8 experts (each wave: 2 expert rows,
-//      lanes stride the hidden dimension in 16-byte chunks; bf16 x bf16 and
-//      fp32 x fp32 products are exact in fp64, so only the summation rounds);
+// Grid: (ceil(N/8) expert groups) x (ceil(T/TT) token tiles), 512 threads (8 waves).
+//   1. every block: fp64 logits of TT tokens x 8 experts.  The block stages its
+//      TT token rows in LDS; each wave owns one expert row and loads all of its
+//      16-byte chunks at once, so the step costs about one memory round trip.
+//      bf16 x bf16 and fp32 x fp32 products are exact in fp64, so only the
+//      summation rounds;
 //   2. the last block of a token tile to finish: softmax and top-K of its tokens
 //      (one wave per token, wave-wide argmax with the lower id winning ties),
 //      gate scores, confidence and class;
@@ -23,9 +25,11 @@
 namespace spice {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxKeys = 3 * SPICE_MAX_EXPERTS;
+constexpr int kKeysPerThread = (kMaxKeys + kThreads - 1) / kThreads;
+constexpr int kMaxRowChunks = 16;  // 16-byte chunks of a router row per lane (d*es <= 16 KiB)
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
@@ -38,6 +42,14 @@ struct Chunk;
 template <>
 struct Chunk<SPICE_BF16> {
     static constexpr int n = 8;
+    __device__ __forceinline__ static void widen(uint4 q, double* v) {
+        const uint32_t w[4] = {q.x, q.y, q.z, q.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            v[2 * i] = (double)bf16_bits_to_float(w[i] & 0xFFFFu);
+            v[2 * i + 1] = (double)bf16_bits_to_float(w[i] >> 16);
+        }
+    }
     __device__ __forceinline__ static void load(const void* base, size_t elem, double* v) {
         const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
         const uint32_t w[4] = {q.x, q.y, q.z, q.w};
@@ -52,6 +64,10 @@ struct Chunk<SPICE_BF16> {
 template <>
 struct Chunk<SPICE_F32> {
     static constexpr int n = 4;
+    __device__ __forceinline__ static void widen(uint4 q, double* v) {
+        v[0] = __uint_as_float(q.x); v[1] = __uint_as_float(q.y);
+        v[2] = __uint_as_float(q.z); v[3] = __uint_as_float(q.w);
+    }
     __device__ __forceinline__ static void load(const void* base, size_t elem, double* v) {
         const float4 q = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + elem);
         v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
@@ -64,19 +80,23 @@ __device__ __forceinline__ double wave_sum_lane0(double v) {
     return __shfl(v, 0);  // every lane takes lane 0's association order
 }
 
+// The block barrier orders every thread's stores before thread 0's device-scope
+// release fence (one L2 write-back per block, not per wave); the last block's
+// thread 0 takes the acquire fence before the barrier releases the others.
 __device__ __forceinline__ bool is_last_arrival(uint32_t* counter, uint32_t n_expected, int* s_flag) {
-    __threadfence();
     __syncthreads();
     if (threadIdx.x == 0) {
+        __threadfence();
         uint32_t prev = atomicAdd(counter, 1u);
         const bool last = (prev == n_expected - 1);
-        if (last) atomicExch(counter, 0u);
+        if (last) {
+            atomicExch(counter, 0u);
+            __threadfence();
+        }
         *s_flag = last ? 1 : 0;
     }
     __syncthreads();
-    const bool last = *s_flag != 0;
-    if (last) __threadfence();
-    return last;
+    return *s_flag != 0;
 }
 
 // Step 2 for one token: wave-wide softmax over N logits, K rounds of argmax.
@@ -171,12 +191,12 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
     }
     __syncthreads();
 
-    // Block-wide exclusive scan over keys; thread `tid` owns keys 3*tid .. 3*tid+2.
+    // Block-wide exclusive scan over keys; thread `tid` owns kKeysPerThread consecutive keys.
     int tot = 0;
-    int cnt[3];
+    int cnt[kKeysPerThread];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-        const int key = 3 * tid + q;
+    for (int q = 0; q < kKeysPerThread; ++q) {
+        const int key = kKeysPerThread * tid + q;
         int v = 0;
         if (key < NK)
             for (int ww = 0; ww < kWaves; ++ww) v += s_base[ww * NK + key];
@@ -194,8 +214,8 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
     int run = incl - tot;
     for (int ww = 0; ww < w; ++ww) run += s_wsum[ww];
 #pragma unroll
-    for (int q = 0; q < 3; ++q) {
-        const int key = 3 * tid + q;
+    for (int q = 0; q < kKeysPerThread; ++q) {
+        const int key = kKeysPerThread * tid + q;
         if (key < NK) {
             const int c = key / N, e = key - c * N;
             a.offsets[c * (N + 1) + e] = run;
@@ -238,67 +258,94 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
 }
 
 template <int DT>
-__global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a) {
-    __shared__ int s_base[kWaves * kMaxKeys];
-    __shared__ int s_run[kWaves * kMaxKeys];
+__global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int tt_tok) {
+    extern __shared__ __align__(16) unsigned char s_dyn[];
     __shared__ int s_wsum[kWaves];
     __shared__ int s_flag;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
-    const int t0 = blockIdx.y * kRouteTok;
-    const int nt = min(kRouteTok, a.T - t0);
+    const int t0 = blockIdx.y * tt_tok;
+    const int nt = min(tt_tok, a.T - t0);
     constexpr int V = Chunk<DT>::n;
-    const int nchunk = a.d / V;
+    constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
+    const int nchunk = a.d / V;  // 16-byte chunks per row
 
-    // 1. logits for (t0 .. t0+nt) x (2 experts of this wave)
-    for (int pe = 0; pe < 2; ++pe) {
-        const int e = blockIdx.x * kRouteExp + w * 2 + pe;
-        if (e >= a.N) break;
+    // 1a. this wave's router row: every chunk it owns, loaded at once
+    const int e = blockIdx.x * kRouteExp + w;
+    uint4 wrow[kMaxRowChunks];
+    if (e < a.N) {
+#pragma unroll
+        for (int i = 0; i < kMaxRowChunks; ++i) {
+            const int c = lane + 64 * i;
+            if (c < nchunk)
+                wrow[i] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.wg) +
+                                                          ((size_t)e * a.d + (size_t)c * V) * es);
+        }
+    }
+    // 1b. the block's token rows into LDS
+    uint4* s_x = reinterpret_cast<uint4*>(s_dyn);
+    for (int i = threadIdx.x; i < nt * nchunk; i += kThreads) {
+        const int tok = i / nchunk, c = i - tok * nchunk;
+        s_x[i] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.x) +
+                                                  ((size_t)(t0 + tok) * a.d + (size_t)c * V) * es);
+    }
+    __syncthreads();
+    if (e < a.N) {
         double acc[kRouteTok];
 #pragma unroll
         for (int i = 0; i < kRouteTok; ++i) acc[i] = 0.0;
-        for (int c = lane; c < nchunk; c += 64) {
-            double wv[V];
-            Chunk<DT>::load(a.wg, (size_t)e * a.d + (size_t)c * V, wv);
 #pragma unroll
-            for (int i = 0; i < kRouteTok; ++i) {
-                if (i < nt) {
-                    double xv[V];
-                    Chunk<DT>::load(a.x, (size_t)(t0 + i) * a.d + (size_t)c * V, xv);
+        for (int i = 0; i < kMaxRowChunks; ++i) {
+            const int c = lane + 64 * i;
+            if (c < nchunk) {
+                double wv[V];
+                Chunk<DT>::widen(wrow[i], wv);
 #pragma unroll
-                    for (int j = 0; j < V; ++j) acc[i] += xv[j] * wv[j];
+                for (int tok = 0; tok < kRouteTok; ++tok) {
+                    if (tok < nt) {
+                        double xv[V];
+                        Chunk<DT>::widen(s_x[tok * nchunk + c], xv);
+#pragma unroll
+                        for (int j = 0; j < V; ++j) acc[tok] += xv[j] * wv[j];
+                    }
                 }
             }
         }
         const double b = a.bias ? (double)a.bias[e] : 0.0;
 #pragma unroll
-        for (int i = 0; i < kRouteTok; ++i) {
-            if (i < nt) {
-                const double zi = wave_sum_lane0(acc[i]) + b;
+        for (int tok = 0; tok < kRouteTok; ++tok) {
+            if (tok < nt) {
+                const double zi = wave_sum_lane0(acc[tok]) + b;
                 if (lane == 0) {
-                    a.logits_ws[(size_t)(t0 + i) * a.N + e] = zi;
-                    if (a.logits_out) a.logits_out[(size_t)(t0 + i) * a.N + e] = zi;
+                    a.logits_ws[(size_t)(t0 + tok) * a.N + e] = zi;
+                    if (a.logits_out) a.logits_out[(size_t)(t0 + tok) * a.N + e] = zi;
                 }
             }
         }
     }
 
-    // 2. the last expert group of this token tile runs the gating
+    // 2. the last expert group of this token tile runs the gating (one wave per token)
     if (!is_last_arrival(&a.ctrl[kWordTileCounters + blockIdx.y], gridDim.x, &s_flag)) return;
     for (int i = w; i < nt; i += kWaves) topk_one_token(a, t0 + i, lane);
 
     // 3. the last token tile buckets every slot
     if (!is_last_arrival(&a.ctrl[kWordRouteDone], gridDim.y, &s_flag)) return;
-    bucket_all(a, s_base, s_run, s_wsum);
+    int* s_base = reinterpret_cast<int*>(s_dyn);
+    bucket_all(a, s_base, s_base + kWaves * kMaxKeys, s_wsum);
 }
 
 }  // namespace
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
-    dim3 grid((a.N + kRouteExp - 1) / kRouteExp, (a.T + kRouteTok - 1) / kRouteTok);
+    const int es = a.dtype == SPICE_BF16 ? 2 : 4;
+    const int tt = route_tokens_per_block(a.d, es);
+    const size_t x_lds = (size_t)tt * a.d * es;
+    const size_t bucket_lds = (size_t)2 * kWaves * kMaxKeys * sizeof(int);
+    const size_t lds = x_lds > bucket_lds ? x_lds : bucket_lds;
+    dim3 grid((a.N + kRouteExp - 1) / kRouteExp, (a.T + tt - 1) / tt);
     if (a.dtype == SPICE_BF16)
-        hipLaunchKernelGGL(route_bucket_kernel<SPICE_BF16>, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(route_bucket_kernel<SPICE_BF16>, grid, dim3(kThreads), lds, s, a, tt);
     else
-        hipLaunchKernelGGL(route_bucket_kernel<SPICE_F32>, grid, dim3(kThreads), 0, s, a);
+        hipLaunchKernelGGL(route_bucket_kernel<SPICE_F32>, grid, dim3(kThreads), lds, s, a, tt);
     return hipGetLastError();
 }
 

@@ -48,6 +48,8 @@ spice_status_t check_cfg(const spice_moe_cfg_t* c) {
     if (c->d % al || c->inter % al || c->shared_inter % al || c->lore_rank % al)
         return fail(SPICE_ERR_UNSUPPORTED, "d, inter, shared_inter and lore_rank must be multiples of " +
                                                std::to_string(al) + " (16-byte vector loads)");
+    if ((int64_t)c->d * (c->dtype == SPICE_BF16 ? 2 : 4) > 16384)
+        return fail(SPICE_ERR_UNSUPPORTED, "hidden rows above 16 KiB (d > 8192 bf16 / 4096 fp32)");
     const int64_t big = (int64_t)std::max({c->d, c->inter, c->shared_inter});
     if (big * SPICE_MAX_TOKENS * 64 > INT64_MAX / 8) return fail(SPICE_ERR_INVALID, "sizes overflow");
     return SPICE_OK;

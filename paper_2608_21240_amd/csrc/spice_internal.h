@@ -13,10 +13,18 @@ namespace spice {
 constexpr int kWordFlags = 0;          // device flags, SPICE_FLAG_* (atomic OR)
 constexpr int kWordRouteDone = 1;      // route tiles finished (last one buckets)
 constexpr int kWordTileCounters = 64;  // one counter per route token tile
-constexpr int kRouteTok = 8;           // tokens per route block
-constexpr int kRouteExp = 8;           // experts per route block (2 per wave)
-static_assert((kWordTileCounters + SPICE_MAX_TOKENS / kRouteTok) * 4 <= SPICE_WS_CONTROL_BYTES,
+constexpr int kRouteTok = 8;           // most tokens per route block
+constexpr int kRouteExp = 8;           // experts per route block (one per wave)
+constexpr int kRouteXLds = 65536;      // LDS bytes for the block's token rows
+constexpr int kRouteMinTok = 4;        // fewest tokens per route block (d * elem <= 16 KiB)
+static_assert((kWordTileCounters + SPICE_MAX_TOKENS / kRouteMinTok) * 4 <= SPICE_WS_CONTROL_BYTES,
               "control region too small");
+
+// Tokens per route block for rows of d elements of es bytes.
+inline int route_tokens_per_block(int d, int es) {
+    const int tt = kRouteXLds / (d * es);
+    return tt > kRouteTok ? kRouteTok : tt;
+}
 
 // Byte offsets of the workspace regions for one (cfg, T).
 struct WsLayout {

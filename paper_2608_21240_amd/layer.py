@@ -129,9 +129,12 @@ class LayerRun:
         s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
         i32 = dict(dtype=torch.int32, device=device)
         f32 = dict(dtype=torch.float32, device=device)
-        self.topk_idx = torch.empty((T, K), **i32)
-        self.topk_w = torch.empty((T, K), **f32)
-        self.slot_class = torch.empty((T, K), dtype=torch.uint8, device=device)
+        # the three routing outputs the exact CPU path reads share one buffer, so one copy stages them
+        sk = T * K
+        self._stage_dev = torch.empty(sk * 9, dtype=torch.uint8, device=device)
+        self.topk_idx = self._stage_dev[: 4 * sk].view(torch.int32).view(T, K)
+        self.topk_w = self._stage_dev[4 * sk: 8 * sk].view(torch.float32).view(T, K)
+        self.slot_class = self._stage_dev[8 * sk:].view(T, K)
         self.offsets = torch.empty((3, N + 1), **i32)
         self.perm = torch.empty(T * K, **i32)
         self.inv_perm = torch.empty(T * K, **i32)
@@ -146,9 +149,10 @@ class LayerRun:
         self.ws = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
         # pinned staging for the exact CPU path
         self.x_host = torch.empty((T, d), dtype=torch_dtype(s.dtype)).pin_memory()
-        self.idx_host = torch.empty((T, K), dtype=torch.int32).pin_memory()
-        self.w_host = torch.empty((T, K), dtype=torch.float32).pin_memory()
-        self.cls_host = torch.empty((T, K), dtype=torch.uint8).pin_memory()
+        self._stage_host = torch.empty(sk * 9, dtype=torch.uint8).pin_memory()
+        self.idx_host = self._stage_host[: 4 * sk].view(torch.int32).view(T, K)
+        self.w_host = self._stage_host[4 * sk: 8 * sk].view(torch.float32).view(T, K)
+        self.cls_host = self._stage_host[8 * sk:].view(T, K)
         self.resid_host = torch.zeros((T, d), dtype=torch.float32).pin_memory()
         self.copy_stream = torch.cuda.Stream(device=device)
         self.e_route = torch.cuda.Event()
@@ -179,16 +183,19 @@ class LayerRun:
         spice.moe_combine(self.cfg, T, self.topk_w, self.slot_class, self.inv_perm, self.y_slots, self.y_shared,
                           resid, self.out)
 
-    def stage_to_host(self, x: torch.Tensor, T: int):
+    def mark_routed(self):
+        """Record the end of routing on the compute stream (the D2H copies wait for it)."""
+        self.e_route.record(torch.cuda.current_stream())
+
+    def stage_to_host(self, x: torch.Tensor, T: int, marked: bool = False):
         """On the copy stream, after routing: D2H of what the exact CPU path reads."""
-        main = torch.cuda.current_stream()
-        self.e_route.record(main)
+        if not marked:
+            self.mark_routed()
         with torch.cuda.stream(self.copy_stream):
             self.copy_stream.wait_event(self.e_route)
             self.x_host[:T].copy_(x[:T], non_blocking=True)
-            self.idx_host[:T].copy_(self.topk_idx[:T], non_blocking=True)
-            self.w_host[:T].copy_(self.topk_w[:T], non_blocking=True)
-            self.cls_host[:T].copy_(self.slot_class[:T], non_blocking=True)
+            # idx / gates / classes of all T rows (rows past T are stale and unread)
+            self._stage_host.copy_(self._stage_dev, non_blocking=True)
             self.e_d2h.record(self.copy_stream)
 
     def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0):
@@ -211,8 +218,10 @@ class LayerRun:
         self.route(L, x, conf, T)
         if "routed" in ev:
             ev["routed"].record()
-        if exact:
+        if exact:  # the host path is the longest leg: its inputs leave the GPU first
             self.stage_to_host(x, T)
+        if "ffn0" in ev:
+            ev["ffn0"].record()
         self.experts(L, x, T, fuse_lore=True)
         if "experts" in ev:
             ev["experts"].record()

@@ -21,7 +21,7 @@ SPICE_F32, SPICE_BF16 = 0, 1
 SPICE_CONF_INPUT, SPICE_CONF_GATE, SPICE_CONF_GATE_RENORM = 0, 1, 2
 SPICE_CLASS_HIT, SPICE_CLASS_LORE, SPICE_CLASS_EXACT = 0, 1, 2
 SPICE_MAX_EXPERTS, SPICE_MAX_TOKENS, SPICE_MAX_LORE_RANK = 256, 65536, 256
-SPICE_WS_CONTROL_BYTES = 65536
+SPICE_WS_CONTROL_BYTES = 131072
 SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
 
 # Every function the header declares (checked against include/spice_moe.h by the tests).
