@@ -103,7 +103,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported (the layer path is single-GPU; "
-              "see the sharding notes in DESIGN.md)", file=sys.stderr)
+              "expert sharding across GPUs is not built)", file=sys.stderr)
         sys.exit(2)
     import torch
 
