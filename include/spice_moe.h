@@ -102,6 +102,22 @@ spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags,
                                      spice_stream_t stream);
 
 /*
+ * Host copies written by moe_route_bucket for the exact CPU path (Sec. 4.3: the hidden
+ * state and the routing decision of the exact misses go to the CPU).  Each pointer is
+ * pinned host memory that the GPU can write (hipHostMalloc, torch's pin_memory), or NULL
+ * to skip that copy; pageable memory is rejected.  The route kernel writes them over
+ * PCIe; they are complete once the stream has passed the call (an event recorded after
+ * it has completed).
+ */
+typedef struct {
+    void* x;               /* [T][d] dtype: the activations */
+    int32_t* topk_idx;     /* [T][K] */
+    float* topk_w;         /* [T][K] */
+    uint8_t* slot_class;   /* [T][K] */
+    int32_t* class_counts; /* [3]: slots per class (HIT, LORE, EXACT) */
+} spice_host_out_t;
+
+/*
  * Steps 1-2: router logits z = x Wg^T (+ bias), softmax over all N, top-K by logit
  * (descending, ties -> lower expert id; Eq. 1), gate g = softmax probability of the
  * chosen expert (Sec. 2.1 weighting), per-slot confidence and class (Sec. 4.2), and a
@@ -120,13 +136,15 @@ spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags,
  *                 HIT, LORE, EXACT; inside a bucket slots keep ascending slot order)
  *   perm          device [T*K] int32 out: perm[pos] = slot id
  *   inv_perm      device [T*K] int32 out: inv_perm[slot] = pos
+ *   host_out      host copies for the CPU path (see spice_host_out_t), or NULL
  */
 spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
                                 const void* w_gate, const float* logit_bias,
                                 const int32_t* resident_slot, const float* conf, double* logits,
                                 int32_t* topk_idx, float* topk_w, uint8_t* slot_class,
-                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, void* ws,
-                                size_t ws_bytes, spice_stream_t stream);
+                                int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                                const spice_host_out_t* host_out, void* ws, size_t ws_bytes,
+                                spice_stream_t stream);
 
 /*
  * Step 3: grouped SwiGLU FFN y = W2 (silu(W1 x) * (W3 x)) (Eq. 6) for every HIT slot,
@@ -170,7 +188,8 @@ spice_status_t lore_surrogate_apply(const spice_moe_cfg_t* cfg, int32_t T, const
  * S(x) + B_e A_e x (Eq. 11) and the CPU outputs merged in (Sec. 4.3).
  *   topk_w, slot_class, inv_perm  device, from moe_route_bucket
  *   y_slots device [T*K][d] fp32, y_shared device [T][d] fp32
- *   resid   device [T][d] fp32 exact-miss residual, or NULL (treated as zero)
+ *   resid   [T][d] fp32 exact-miss residual, or NULL (treated as zero): device memory,
+ *           or pinned host memory (read over PCIe: the CPU result needs no separate copy)
  *   out     device [T][d] dtype out (bf16: round to nearest even); must not alias inputs
  */
 spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w,
@@ -196,6 +215,78 @@ spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, int32_t T, co
                                        const uint8_t* slot_class_host,
                                        const void* const* w13_host, const void* const* w2_host,
                                        float* resid_host, int32_t n_threads);
+
+/*
+ * Expert cache of a decode stack (the stack workload): per layer, the set of routed
+ * experts resident in that layer's slot pool, which the hit test of Sec. 4.2 reads
+ * through resident_slot.  The paper's GPU holds only part of the experts (Sec. 1, 3)
+ * and compares against an LRU-managed cache (Sec. 5); this handle keeps each layer's
+ * pool LRU-managed as follows.  After the layer's call at decode step s:
+ *   1. experts of the call's HIT slots are marked used at s;
+ *   2. experts of its EXACT slots that are not resident are candidates, more EXACT
+ *      slots first, then lower id; LORE misses are never admitted (Sec. 4.2: they need
+ *      no transfer);
+ *   3. each candidate, at most max_admit per call (a bounded copy queue), takes the slot
+ *      whose expert was used longest ago, ties to the lower expert id (an empty slot
+ *      first), never a slot used at s; the new slot counts as used at s;
+ *   4. the admitted weights are copied host -> pool on copy_stream, ordered after the
+ *      work already queued on compute_stream, and the layer's device resident_slot is
+ *      rewritten after them.
+ * Admitted experts are still EXACT (served on the CPU) in step s; they are resident
+ * for the layer's next call, which moe_cache_wait orders after the copies.
+ * A handle is not thread-safe; one host thread drives it.
+ */
+typedef struct spice_cache spice_cache_t;
+
+/*
+ * Create a cache for n_layers layers of the same cfg, each with cfg->n_slots slots.
+ *   w13_host, w2_host host tables [n_layers * N] of host pointers to expert e of layer l
+ *                     at [l*N + e]: [2I][d] and [d][I] (dtype).  Pinned memory lets the
+ *                     copies run asynchronously.  Entries may be NULL for experts that
+ *                     are never admitted or loaded.
+ *   w13_pool, w2_pool host tables [n_layers] of device pool bases ([C][2I][d], [C][d][I])
+ *   resident_slot     host table [n_layers] of device int32 [N] arrays that the cache
+ *                     keeps equal to its state (the moe_route_bucket / FFN input)
+ *   initial_experts   host [n_layers][C] int32: expert in each slot (-1 = empty), each
+ *                     expert at most once per layer; every slot starts "never used"
+ *   load              1: copy the initial experts into the pools and write resident_slot
+ *                     now, on `stream`, and wait for it; 0: the caller has done both
+ *   out               receives the handle
+ * With w13_pool == NULL the handle does the bookkeeping only: no pools, copies or HIP
+ * calls (then w2_pool, resident_slot and the host tables are ignored and load must be 0).
+ * The handle borrows every pointer in the tables until moe_cache_destroy.
+ */
+spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, const void* const* w13_host,
+                                const void* const* w2_host, void* const* w13_pool, void* const* w2_pool,
+                                int32_t* const* resident_slot, const int32_t* initial_experts, int32_t load,
+                                spice_stream_t stream, spice_cache_t** out);
+
+/*
+ * Update layer `layer` after its call at decode step `step` (rules 1-4 above).
+ *   topk_idx_host, slot_class_host  host [T][K]: the call's routing (moe_route_bucket)
+ *   max_admit          admissions allowed in this call (>= 0)
+ *   copy_stream        stream of the host -> pool copies; compute_stream: stream of the
+ *                      layer's kernels (the copies wait for its queued work)
+ *   n_admitted         out: number admitted
+ *   admitted, evicted  host [max_admit] out: admitted experts in order, and the expert
+ *                      each one replaced (-1 = the slot was empty)
+ * Returns INVALID for out-of-range ids or classes, or a NULL host weight of an EXACT
+ * expert; the state is then unchanged.
+ */
+spice_status_t moe_cache_step(spice_cache_t* cache, int32_t layer, int32_t step, int32_t T,
+                              const int32_t* topk_idx_host, const uint8_t* slot_class_host, int32_t max_admit,
+                              spice_stream_t copy_stream, spice_stream_t compute_stream, int32_t* n_admitted,
+                              int32_t* admitted, int32_t* evicted);
+
+/* Make `stream` wait for the layer's outstanding admissions (no-op if none).  Call it
+ * before the layer's next moe_route_bucket. */
+spice_status_t moe_cache_wait(spice_cache_t* cache, int32_t layer, spice_stream_t stream);
+
+/* Host copy of a layer's state: slot_expert[C] and last_use[C] (-1 = never); either may be NULL. */
+spice_status_t moe_cache_state(const spice_cache_t* cache, int32_t layer, int32_t* slot_expert, int32_t* last_use);
+
+/* Wait for outstanding copies and free the handle (NULL is ignored). */
+void moe_cache_destroy(spice_cache_t* cache);
 
 /* Text of a status code, and the last error message of the calling thread. */
 const char* spice_status_string(spice_status_t status);

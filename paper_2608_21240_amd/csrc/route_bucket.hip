@@ -13,6 +13,8 @@
 //   3. the last token tile to finish: stable counting sort of all T*K slots by
 //      key (class, expert) with per-wave histograms, a block scan, and ballot
 //      matching to rank equal keys inside each 64-slot chunk.
+// Optional host copies for the CPU path (x, top-K, gates, classes, class counts)
+// are stored straight into the caller's pinned host memory along the way.
 // "Last block" is decided with an agent-scope atomic counter in the workspace
 // control region after a device fence; the last block resets the counter.
 #include <float.h>
@@ -164,6 +166,9 @@ __device__ void topk_one_token(const RouteArgs& a, int t, int lane) {
         a.topk_idx[s] = my_e;
         a.topk_w[s] = (float)g;
         a.slot_class[s] = cls;
+        if (a.h_idx) a.h_idx[s] = my_e;
+        if (a.h_w) a.h_w[s] = (float)g;
+        if (a.h_cls) a.h_cls[s] = cls;
     }
 }
 
@@ -178,10 +183,11 @@ __device__ __forceinline__ int slot_key(const RouteArgs& a, int s) {
 }
 
 // Step 3: stable counting sort of the T*K slots by key = class*N + expert.
-__device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_wsum) {
+__device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_wsum, int* s_ccount) {
     const int N = a.N, S = a.T * a.K, NK = 3 * N;
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     for (int i = tid; i < kWaves * NK; i += kThreads) { s_base[i] = 0; s_run[i] = 0; }
+    if (tid < 3) s_ccount[tid] = 0;
     __syncthreads();
     const int per = (S + kWaves - 1) / kWaves;
     const int lo = min(S, w * per), hi = min(S, lo + per);
@@ -202,6 +208,7 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
             for (int ww = 0; ww < kWaves; ++ww) v += s_base[ww * NK + key];
         cnt[q] = v;
         tot += v;
+        if (v) atomicAdd(&s_ccount[key / N], v);
     }
     int incl = tot;
 #pragma unroll
@@ -230,6 +237,7 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
         }
     }
     __syncthreads();
+    if (a.h_counts && tid < 3) a.h_counts[tid] = s_ccount[tid];
 
     const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
     for (int base = lo; base < hi; base += 64) {
@@ -261,6 +269,7 @@ template <int DT>
 __global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int tt_tok) {
     extern __shared__ __align__(16) unsigned char s_dyn[];
     __shared__ int s_wsum[kWaves];
+    __shared__ int s_ccount[3];
     __shared__ int s_flag;
     const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
     const int t0 = blockIdx.y * tt_tok;
@@ -283,10 +292,13 @@ __global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int
     }
     // 1b. the block's token rows into LDS
     uint4* s_x = reinterpret_cast<uint4*>(s_dyn);
+    const bool mirror_x = a.hx != nullptr && blockIdx.x == 0;  // one expert group copies x to the host
     for (int i = threadIdx.x; i < nt * nchunk; i += kThreads) {
         const int tok = i / nchunk, c = i - tok * nchunk;
-        s_x[i] = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.x) +
-                                                  ((size_t)(t0 + tok) * a.d + (size_t)c * V) * es);
+        const size_t off = ((size_t)(t0 + tok) * a.d + (size_t)c * V) * es;
+        const uint4 q = *reinterpret_cast<const uint4*>(static_cast<const char*>(a.x) + off);
+        s_x[i] = q;
+        if (mirror_x) *reinterpret_cast<uint4*>(static_cast<char*>(a.hx) + off) = q;
     }
     __syncthreads();
     if (e < a.N) {
@@ -330,7 +342,7 @@ __global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int
     // 3. the last token tile buckets every slot
     if (!is_last_arrival(&a.ctrl[kWordRouteDone], gridDim.y, &s_flag)) return;
     int* s_base = reinterpret_cast<int*>(s_dyn);
-    bucket_all(a, s_base, s_base + kWaves * kMaxKeys, s_wsum);
+    bucket_all(a, s_base, s_base + kWaves * kMaxKeys, s_wsum, s_ccount);
 }
 
 }  // namespace

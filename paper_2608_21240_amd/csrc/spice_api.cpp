@@ -77,6 +77,29 @@ bool overlaps(const void* a, size_t an, const void* b, size_t bn) {
     return a0 < b0 + bn && b0 < a0 + an;
 }
 
+// Address a kernel may use for a caller buffer that must be pinned host memory
+// (host_only) or either device or pinned host memory.  Pageable memory would make
+// the kernel fault, so it is rejected here.
+spice_status_t gpu_address(const void* p, bool host_only, const char* name, void** dev) {
+    hipPointerAttribute_t at{};
+    const hipError_t e = hipPointerGetAttributes(&at, p);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(SPICE_ERR_INVALID, std::string(name) + ": not device or pinned host memory (" +
+                                           hipGetErrorString(e) + ")");
+    }
+    if (at.type == hipMemoryTypeHost) {
+        *dev = at.devicePointer ? at.devicePointer : const_cast<void*>(p);
+        return SPICE_OK;
+    }
+    if (!host_only && (at.type == hipMemoryTypeDevice || at.type == hipMemoryTypeManaged)) {
+        *dev = const_cast<void*>(p);
+        return SPICE_OK;
+    }
+    return fail(SPICE_ERR_INVALID, std::string(name) + (host_only ? ": must be pinned host memory"
+                                                                   : ": not device or pinned host memory"));
+}
+
 #define SPICE_REQUIRE(ptr, name) \
     if (!(ptr)) return fail(SPICE_ERR_INVALID, name " is NULL")
 
@@ -143,8 +166,8 @@ spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags,
 spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
                                 const float* logit_bias, const int32_t* resident_slot, const float* conf,
                                 double* logits, int32_t* topk_idx, float* topk_w, uint8_t* slot_class,
-                                int32_t* offsets, int32_t* perm, int32_t* inv_perm, void* ws, size_t ws_bytes,
-                                spice_stream_t stream) {
+                                int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                                const spice_host_out_t* host_out, void* ws, size_t ws_bytes, spice_stream_t stream) {
     SPICE_TRY_BEGIN
     spice_status_t st = check_cfg(cfg);
     if (st != SPICE_OK) return st;
@@ -172,6 +195,29 @@ spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const voi
     a.topk_idx = topk_idx; a.topk_w = topk_w; a.slot_class = slot_class;
     a.offsets = offsets; a.perm = perm; a.inv_perm = inv_perm;
     a.ctrl = reinterpret_cast<uint32_t*>(wsb);
+    if (host_out) {
+        void* d = nullptr;
+        if (host_out->x) {
+            if ((st = gpu_address(host_out->x, true, "host_out.x", &d)) != SPICE_OK) return st;
+            a.hx = d;
+        }
+        if (host_out->topk_idx) {
+            if ((st = gpu_address(host_out->topk_idx, true, "host_out.topk_idx", &d)) != SPICE_OK) return st;
+            a.h_idx = static_cast<int32_t*>(d);
+        }
+        if (host_out->topk_w) {
+            if ((st = gpu_address(host_out->topk_w, true, "host_out.topk_w", &d)) != SPICE_OK) return st;
+            a.h_w = static_cast<float*>(d);
+        }
+        if (host_out->slot_class) {
+            if ((st = gpu_address(host_out->slot_class, true, "host_out.slot_class", &d)) != SPICE_OK) return st;
+            a.h_cls = static_cast<uint8_t*>(d);
+        }
+        if (host_out->class_counts) {
+            if ((st = gpu_address(host_out->class_counts, true, "host_out.class_counts", &d)) != SPICE_OK) return st;
+            a.h_counts = static_cast<int32_t*>(d);
+        }
+    }
     hipError_t e = spice::launch_route_bucket(a, stream);
     if (e != hipSuccess) return hip_fail(e, "moe_route_bucket");
     return SPICE_OK;
@@ -270,10 +316,12 @@ spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* t
     if (overlaps(out, osz, y_slots, fsz * c.top_k) || overlaps(out, osz, y_shared, fsz) ||
         overlaps(out, osz, resid, fsz) || overlaps(out, osz, topk_w, (size_t)T * c.top_k * sizeof(float)))
         return fail(SPICE_ERR_INVALID, "moe_combine: out aliases an input");
+    void* resid_dev = nullptr;
+    if (resid && (st = gpu_address(resid, false, "moe_combine: resid", &resid_dev)) != SPICE_OK) return st;
     spice::CombineArgs a{};
     a.T = T; a.d = c.d; a.K = c.top_k; a.dtype = c.dtype;
     a.topk_w = topk_w; a.slot_class = slot_class; a.inv_perm = inv_perm; a.y_slots = y_slots;
-    a.y_shared = y_shared; a.resid = resid; a.out = out;
+    a.y_shared = y_shared; a.resid = static_cast<const float*>(resid_dev); a.out = out;
     hipError_t e = spice::launch_combine(a, stream);
     if (e != hipSuccess) return hip_fail(e, "moe_combine");
     return SPICE_OK;

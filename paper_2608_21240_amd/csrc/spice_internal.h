@@ -56,6 +56,12 @@ struct RouteArgs {
     int32_t* perm;
     int32_t* inv_perm;
     uint32_t* ctrl;       // workspace control words
+    // device-visible addresses of the caller's pinned host copies (each nullable)
+    void* hx;
+    int32_t* h_idx;
+    float* h_w;
+    uint8_t* h_cls;
+    int32_t* h_counts;
 };
 
 struct FfnArgs {

@@ -6,9 +6,9 @@ block and every expert's LoRE factors, and keeps the non-resident experts on
 the host for the exact CPU path.  ``LayerRun`` owns the per-call buffers and
 runs the path in the order the paper describes (Sec. 4.3):
 
-    stream s   : route+bucket -> grouped FFN (+LoRE) ............ wait(e_h2d) -> combine
-    copy stream:        wait(route) -> D2H x, idx, gates, classes    H2D resid -> e_h2d
-    host       :                       sync -> exact residual (CPU threads)
+    stream : route+bucket (also writes x and the routing into pinned host memory)
+             -> grouped FFN (+LoRE) ........................ -> combine (reads resid over PCIe)
+    host   :        wait(route) -> exact residual on CPU threads -> resid (pinned) ^
 
 Every arithmetic step runs inside libspice_moe (HIP kernels or its host path).
 """
@@ -129,42 +129,41 @@ class LayerRun:
         s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
         i32 = dict(dtype=torch.int32, device=device)
         f32 = dict(dtype=torch.float32, device=device)
-        # the three routing outputs the exact CPU path reads share one buffer, so one copy stages them
-        sk = T * K
-        self._stage_dev = torch.empty(sk * 9, dtype=torch.uint8, device=device)
-        self.topk_idx = self._stage_dev[: 4 * sk].view(torch.int32).view(T, K)
-        self.topk_w = self._stage_dev[4 * sk: 8 * sk].view(torch.float32).view(T, K)
-        self.slot_class = self._stage_dev[8 * sk:].view(T, K)
+        self.topk_idx = torch.empty((T, K), **i32)
+        self.topk_w = torch.empty((T, K), **f32)
+        self.slot_class = torch.empty((T, K), dtype=torch.uint8, device=device)
         self.offsets = torch.empty((3, N + 1), **i32)
         self.perm = torch.empty(T * K, **i32)
         self.inv_perm = torch.empty(T * K, **i32)
         self.logits = torch.empty((T, N), dtype=torch.float64, device=device) if keep_logits else None
         self.y_slots = torch.zeros((T * K, d), **f32)
         self.y_shared = torch.zeros((T, d), **f32)
-        self.resid = torch.zeros((T, d), **f32)
         self.out = torch.empty((T, d), dtype=torch_dtype(s.dtype), device=device)
         self.ws_bytes = spice.spice_workspace_bytes(self.cfg, T)
         if self.ws_bytes == 0:
             raise ValueError(f"invalid configuration for the library: {spice.last_error()}")
         self.ws = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
-        # pinned staging for the exact CPU path
+        # pinned host memory of the exact CPU path: the route kernel writes x and the
+        # routing here, the CPU writes the residual that the combine kernel reads
         self.x_host = torch.empty((T, d), dtype=torch_dtype(s.dtype)).pin_memory()
-        self._stage_host = torch.empty(sk * 9, dtype=torch.uint8).pin_memory()
-        self.idx_host = self._stage_host[: 4 * sk].view(torch.int32).view(T, K)
-        self.w_host = self._stage_host[4 * sk: 8 * sk].view(torch.float32).view(T, K)
-        self.cls_host = self._stage_host[8 * sk:].view(T, K)
-        self.resid_host = torch.zeros((T, d), dtype=torch.float32).pin_memory()
-        self.copy_stream = torch.cuda.Stream(device=device)
+        self.idx_host = torch.empty((T, K), dtype=torch.int32).pin_memory()
+        self.w_host = torch.empty((T, K), dtype=torch.float32).pin_memory()
+        self.cls_host = torch.empty((T, K), dtype=torch.uint8).pin_memory()
+        self.counts_host = torch.zeros(3, dtype=torch.int32).pin_memory()
+        self.resid = torch.zeros((T, d), dtype=torch.float32).pin_memory()
+        self.host_out = spice.host_out(self.x_host, self.idx_host, self.w_host, self.cls_host, self.counts_host)
         self.e_route = torch.cuda.Event()
-        self.e_d2h = torch.cuda.Event()
-        self.e_h2d = torch.cuda.Event()
 
     # -- the steps, each one C-ABI call ------------------------------------------------
-    def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None):
+    def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
+              to_host: bool = True):
+        """Routing + bucketing; with to_host the kernel also fills the pinned host copies,
+        and e_route marks the end of the call on the stream."""
         T = self.T if T is None else T
         spice.moe_route_bucket(self.cfg, T, x, L.wg, L.bias, L.resident_slot, conf, self.logits, self.topk_idx,
-                               self.topk_w, self.slot_class, self.offsets, self.perm, self.inv_perm, self.ws,
-                               self.ws_bytes)
+                               self.topk_w, self.slot_class, self.offsets, self.perm, self.inv_perm,
+                               self.host_out if to_host else None, self.ws, self.ws_bytes)
+        self.e_route.record(torch.cuda.current_stream())
 
     def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
         T = self.T if T is None else T
@@ -183,30 +182,11 @@ class LayerRun:
         spice.moe_combine(self.cfg, T, self.topk_w, self.slot_class, self.inv_perm, self.y_slots, self.y_shared,
                           resid, self.out)
 
-    def mark_routed(self):
-        """Record the end of routing on the compute stream (the D2H copies wait for it)."""
-        self.e_route.record(torch.cuda.current_stream())
-
-    def stage_to_host(self, x: torch.Tensor, T: int, marked: bool = False):
-        """On the copy stream, after routing: D2H of what the exact CPU path reads."""
-        if not marked:
-            self.mark_routed()
-        with torch.cuda.stream(self.copy_stream):
-            self.copy_stream.wait_event(self.e_route)
-            self.x_host[:T].copy_(x[:T], non_blocking=True)
-            # idx / gates / classes of all T rows (rows past T are stale and unread)
-            self._stage_host.copy_(self._stage_dev, non_blocking=True)
-            self.e_d2h.record(self.copy_stream)
-
     def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0):
-        """Wait for the staged routing results, run the CPU residual, H2D it on the copy stream."""
-        self.e_d2h.synchronize()
+        """Wait for the route kernel's host copies, then the CPU residual into self.resid."""
+        self.e_route.synchronize()
         spice.moe_exact_residual_host(self.cfg, T, self.x_host, self.idx_host, self.w_host, self.cls_host,
-                                      L.host_w13, L.host_w2, self.resid_host, n_threads)
-        with torch.cuda.stream(self.copy_stream):
-            self.resid[:T].copy_(self.resid_host[:T], non_blocking=True)
-            self.e_h2d.record(self.copy_stream)
-        torch.cuda.current_stream().wait_event(self.e_h2d)
+                                      L.host_w13, L.host_w2, self.resid, n_threads)
 
     def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
                 exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None):
@@ -215,11 +195,9 @@ class LayerRun:
         ev = events or {}
         if "start" in ev:
             ev["start"].record()
-        self.route(L, x, conf, T)
+        self.route(L, x, conf, T, to_host=exact)
         if "routed" in ev:
             ev["routed"].record()
-        if exact:  # the host path is the longest leg: its inputs leave the GPU first
-            self.stage_to_host(x, T)
         if "ffn0" in ev:
             ev["ffn0"].record()
         self.experts(L, x, T, fuse_lore=True)

@@ -28,7 +28,8 @@ SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
 EXPORTS = (
     "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
     "moe_route_bucket", "moe_expert_ffn_grouped", "lore_surrogate_apply", "moe_combine",
-    "moe_exact_residual_host", "spice_status_string", "spice_last_error",
+    "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
+    "moe_cache_destroy", "spice_status_string", "spice_last_error",
 )
 
 
@@ -43,6 +44,16 @@ class spice_moe_cfg_t(ctypes.Structure):
                 ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
                 ("n_slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32),
                 ("conf_mode", ctypes.c_int32), ("tau", ctypes.c_float)]
+
+
+class spice_host_out_t(ctypes.Structure):
+    _fields_ = [("x", ctypes.c_void_p), ("topk_idx", ctypes.c_void_p), ("topk_w", ctypes.c_void_p),
+                ("slot_class", ctypes.c_void_p), ("class_counts", ctypes.c_void_p)]
+
+
+def host_out(x=None, topk_idx=None, topk_w=None, slot_class=None, class_counts=None) -> spice_host_out_t:
+    """Pinned host buffers (tensors, arrays or addresses) for moe_route_bucket's host copies."""
+    return spice_host_out_t(_p(x), _p(topk_idx), _p(topk_w), _p(slot_class), _p(class_counts))
 
 
 def make_cfg(shape, n_slots: int, tau: float = 0.5, conf_mode: int = SPICE_CONF_INPUT,
@@ -66,11 +77,17 @@ def lib() -> ctypes.CDLL:
             "spice_workspace_bytes": (_Z, [C, _I]),
             "spice_workspace_init": (_I, [_P, _Z, _P]),
             "spice_workspace_flags": (_I, [_P, _Z, ctypes.POINTER(ctypes.c_uint32), _I, _P]),
-            "moe_route_bucket": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+            "moe_route_bucket": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                      ctypes.POINTER(spice_host_out_t), _P, _Z, _P]),
             "moe_expert_ffn_grouped": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
             "lore_surrogate_apply": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
             "moe_combine": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
             "moe_exact_residual_host": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I]),
+            "moe_cache_create": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _I, _P, ctypes.POINTER(_P)]),
+            "moe_cache_step": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, ctypes.POINTER(_I), _P, _P]),
+            "moe_cache_wait": (_I, [_P, _I, _P]),
+            "moe_cache_state": (_I, [_P, _I, _P, _P]),
+            "moe_cache_destroy": (None, [_P]),
             "spice_status_string": (ctypes.c_char_p, [_I]),
             "spice_last_error": (ctypes.c_char_p, []),
         }
@@ -135,11 +152,12 @@ def spice_workspace_flags(ws, ws_bytes: int, clear: bool = False, stream=None) -
 
 
 def moe_route_bucket(cfg, T, x, w_gate, logit_bias, resident_slot, conf, logits, topk_idx, topk_w, slot_class,
-                     offsets, perm, inv_perm, ws, ws_bytes, stream=None) -> None:
+                     offsets, perm, inv_perm, host_out: Optional[spice_host_out_t], ws, ws_bytes,
+                     stream=None) -> None:
     _check("moe_route_bucket", lib().moe_route_bucket(
         ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(logits),
-        _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm), _p(ws), ws_bytes,
-        _stream(stream)))
+        _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm),
+        None if host_out is None else ctypes.byref(host_out), _p(ws), ws_bytes, _stream(stream)))
 
 
 def moe_expert_ffn_grouped(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared,
@@ -170,3 +188,74 @@ def moe_exact_residual_host(cfg, T, x_host, topk_idx_host, topk_w_host, slot_cla
     _check("moe_exact_residual_host", lib().moe_exact_residual_host(
         ctypes.byref(cfg), T, _p(x_host), _p(topk_idx_host), _p(topk_w_host), _p(slot_class_host), t13, t2,
         _p(resid_host), n_threads))
+
+
+def _table(items, n: int):
+    """ctypes array of n addresses (None -> NULL)."""
+    items = list(items)
+    if len(items) != n:
+        raise ValueError(f"table needs {n} entries, got {len(items)}")
+    return (ctypes.c_void_p * n)(*[_p(a) for a in items])
+
+
+class ExpertCache:
+    """Handle of moe_cache_create (bookkeeping only when w13_pool is None)."""
+
+    def __init__(self, cfg: spice_moe_cfg_t, n_layers: int, initial_experts, w13_host=None, w2_host=None,
+                 w13_pool=None, w2_pool=None, resident_slot=None, load: bool = False, stream=None):
+        import numpy as np
+
+        self.cfg, self.L, self.C = cfg, n_layers, cfg.n_slots
+        self.device = w13_pool is not None
+        init = np.ascontiguousarray(initial_experts, dtype=np.int32).reshape(n_layers, cfg.n_slots)
+        self._keep = [init]
+        args = [None] * 5
+        if w13_pool is not None:
+            LN = n_layers * cfg.n_experts
+            args = [_table(w13_host, LN), _table(w2_host, LN), _table(w13_pool, n_layers),
+                    _table(w2_pool, n_layers), _table(resident_slot, n_layers)]
+            self._keep += [w13_host, w2_host, w13_pool, w2_pool, resident_slot, args]
+        h = ctypes.c_void_p(None)
+        _check("moe_cache_create", lib().moe_cache_create(
+            ctypes.byref(cfg), n_layers, args[0], args[1], args[2], args[3], args[4], init.ctypes.data, int(load),
+            _stream(stream) if w13_pool is not None else None, ctypes.byref(h)))
+        self.h = h.value
+
+    def step(self, layer: int, step: int, idx, cls, max_admit: int, copy_stream=None, compute_stream=None):
+        """-> (admitted, evicted) as lists."""
+        import numpy as np
+
+        idx = np.ascontiguousarray(idx, dtype=np.int32)
+        cls = np.ascontiguousarray(cls, dtype=np.uint8)
+        T = idx.shape[0] if idx.ndim == 2 else idx.size // self.cfg.top_k
+        n = ctypes.c_int32(0)
+        adm = np.empty(max(max_admit, 1), np.int32)
+        ev = np.empty(max(max_admit, 1), np.int32)
+        dev = self.device
+        _check("moe_cache_step", lib().moe_cache_step(
+            self.h, layer, step, T, idx.ctypes.data, cls.ctypes.data, max_admit,
+            _stream(copy_stream) if dev else None, _stream(compute_stream) if dev else None, ctypes.byref(n),
+            adm.ctypes.data, ev.ctypes.data))
+        return adm[:n.value].tolist(), ev[:n.value].tolist()
+
+    def wait(self, layer: int, stream=None) -> None:
+        _check("moe_cache_wait", lib().moe_cache_wait(self.h, layer, _stream(stream)))
+
+    def state(self, layer: int):
+        import numpy as np
+
+        se = np.empty(self.C, np.int32)
+        lu = np.empty(self.C, np.int32)
+        _check("moe_cache_state", lib().moe_cache_state(self.h, layer, se.ctypes.data, lu.ctypes.data))
+        return se, lu
+
+    def close(self) -> None:
+        if getattr(self, "h", None):
+            lib().moe_cache_destroy(self.h)
+            self.h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -40,21 +40,27 @@ def rng(*key: int) -> np.random.Generator:
     return np.random.default_rng([int(k) & 0xFFFFFFFF for k in key])
 
 
-def f32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
-    """Round fp32 to bf16 (round to nearest, ties to even); returns uint16 bits."""
-    u = np.ascontiguousarray(a, dtype=np.float32).view(np.uint32)
-    bias = ((u >> np.uint32(16)) & np.uint32(1)) + np.uint32(0x7FFF)
-    return ((u + bias) >> np.uint32(16)).astype(np.uint16)
+def f32_to_bf16_bits(a: np.ndarray, overwrite: bool = False) -> np.ndarray:
+    """Round fp32 to bf16 (round to nearest, ties to even); returns uint16 bits.
+    overwrite=True lets the (float32, contiguous) input serve as scratch."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32) if overwrite else a.view(np.uint32).copy()
+    bias = u >> np.uint32(16)
+    bias &= np.uint32(1)
+    bias += np.uint32(0x7FFF)
+    u += bias
+    u >>= np.uint32(16)
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
     return (np.ascontiguousarray(b, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32)
 
 
-def to_storage(a32: np.ndarray, dtype: int) -> np.ndarray:
+def to_storage(a32: np.ndarray, dtype: int, overwrite: bool = False) -> np.ndarray:
     """fp32 draw -> storage array (float32, or uint16 bf16 bits)."""
     if dtype == DTYPE_BF16:
-        return f32_to_bf16_bits(a32)
+        return f32_to_bf16_bits(a32, overwrite=overwrite)
     return np.ascontiguousarray(a32, dtype=np.float32)
 
 
@@ -67,7 +73,7 @@ def _normal(key: Tuple[int, ...], shape, std: float, dtype: int) -> np.ndarray:
     a = rng(*key).standard_normal(size=shape, dtype=np.float32)
     if std != 1.0:
         a *= np.float32(std)
-    return to_storage(a, dtype)
+    return to_storage(a, dtype, overwrite=True)
 
 
 def _key(wl: Workload, layer: int, tensor: int, index: int = 0) -> Tuple[int, ...]:

@@ -77,9 +77,7 @@ class Case:
         if fused:
             R.forward(self.dev, xd, conf, self.T, exact=exact, n_threads=n_threads)
         else:
-            R.route(self.dev, xd, conf, self.T)
-            if exact:
-                R.stage_to_host(xd, self.T)
+            R.route(self.dev, xd, conf, self.T, to_host=exact)
             R.experts(self.dev, xd, self.T, fuse_lore=False)
             R.lore(self.dev, xd, self.T)
             if exact:

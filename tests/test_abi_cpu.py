@@ -16,7 +16,7 @@ DUMMY = 0x1000  # never dereferenced: every case below fails validation first
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(?:spice_status_t|size_t|const char\*)\s+(\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(?:spice_status_t|size_t|void|const char\*)\s+(\w+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
@@ -35,7 +35,7 @@ def cfg(**kw):
     return c
 
 
-def route(c, T=4, ws_bytes=None, conf=DUMMY, **ptrs):
+def route(c, T=4, ws_bytes=None, conf=DUMMY, host_out=None, **ptrs):
     p = dict(x=DUMMY, w_gate=DUMMY, resident_slot=DUMMY, topk_idx=DUMMY, topk_w=DUMMY, slot_class=DUMMY,
              offsets=DUMMY, perm=DUMMY, inv_perm=DUMMY, ws=DUMMY)
     p.update(ptrs)
@@ -43,7 +43,8 @@ def route(c, T=4, ws_bytes=None, conf=DUMMY, **ptrs):
         ws_bytes = spice.spice_workspace_bytes(c, T) if spice.spice_workspace_bytes(c, T) else 1 << 40
     return spice.lib().moe_route_bucket(ctypes.byref(c), T, p["x"], p["w_gate"], None, p["resident_slot"], conf,
                                         None, p["topk_idx"], p["topk_w"], p["slot_class"], p["offsets"], p["perm"],
-                                        p["inv_perm"], p["ws"], ws_bytes, None)
+                                        p["inv_perm"], None if host_out is None else ctypes.byref(host_out),
+                                        p["ws"], ws_bytes, None)
 
 
 @pytest.mark.parametrize("field,value,status", [
@@ -72,7 +73,7 @@ def test_token_count_rules():
     assert route(cfg(), T=spice.SPICE_MAX_TOKENS + 1) == spice.SPICE_ERR_UNSUPPORTED
     # T == 0 is a no-op even with NULL buffers
     z = spice.lib().moe_route_bucket(ctypes.byref(cfg()), 0, None, None, None, None, None, None, None, None, None,
-                                     None, None, None, None, 0, None)
+                                     None, None, None, None, None, 0, None)
     assert z == spice.SPICE_OK
 
 
@@ -114,3 +115,14 @@ def test_ffn_lore_combine_validation():
 def test_status_strings():
     assert spice.spice_status_string(spice.SPICE_ERR_WORKSPACE) == "SPICE_ERR_WORKSPACE"
     assert spice.spice_status_string(12345) == "unknown spice_status_t"
+
+
+def test_pageable_host_copies_are_rejected():
+    """The route kernel writes host copies over PCIe: pageable memory would fault, so it is refused."""
+    import numpy as np
+
+    buf = np.zeros(1 << 16, np.uint8)
+    for field in ("x", "topk_idx", "topk_w", "slot_class", "class_counts"):
+        ho = spice.host_out(**{field: buf})
+        assert route(cfg(), host_out=ho) == spice.SPICE_ERR_INVALID
+        assert "host_out." + field in spice.last_error()

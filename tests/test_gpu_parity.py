@@ -210,3 +210,19 @@ def test_repeat_runs_are_bit_identical():
     for k in g1:
         if k != "flags":
             assert np.array_equal(g1[k], g2[k]), k
+
+
+@pytest.mark.parametrize("shape,T,R", [(RAGGED_BF16, 37, 6), (RAGGED_F32, 41, 4)])
+def test_host_copies_match_device_outputs(shape, T, R):
+    """The route kernel's pinned-host copies equal its device outputs and the input x;
+    the class counts equal the histogram of the classes."""
+    say(f"host copies d={shape.d} T={T}")
+    c = Case(small_wl(shape, T, R))
+    c.run_gpu()
+    run = c.run
+    assert np.array_equal(run.idx_host[:T].numpy(), c.g["idx"])
+    assert np.array_equal(run.w_host[:T].numpy(), c.g["w"])
+    assert np.array_equal(run.cls_host[:T].numpy(), c.g["cls"])
+    assert run.counts_host.tolist() == np.bincount(c.g["cls"].reshape(-1), minlength=3).tolist()
+    from parity import to_np
+    assert np.array_equal(to_np(run.x_host[:T]), c.x)
