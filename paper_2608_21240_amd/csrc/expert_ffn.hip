@@ -513,7 +513,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 
 }  // namespace
 
-hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s) {
+hipError_t launch_expert_ffn(const FfnArgs& f, hipStream_t s) {
+    FfnArgs a = f;
+    if ((a.groups & (kDoHit | kDoShared)) && expert_gemm_applies(a)) {
+        // many tokens: the HIT experts and the shared block as MFMA GEMMs; LoRE below
+        const hipError_t e = launch_expert_gemm(a, (a.groups & kDoHit) != 0, (a.groups & kDoShared) != 0, s);
+        if (e != hipSuccess) return e;
+        a.groups &= kDoLore;
+    }
     const bool hit = (a.groups & kDoHit) != 0;
     const bool shared = (a.groups & kDoShared) != 0 && a.Is > 0;
     const bool lore = (a.groups & kDoLore) != 0 && a.r > 0;

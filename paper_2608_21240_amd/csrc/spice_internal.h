@@ -95,6 +95,30 @@ struct CombineArgs {
     void* out;
 };
 
+// Grouped MFMA GEMMs of the HIT experts and the shared block for large token
+// counts (bf16; used by launch_expert_ffn when expert_gemm_applies).
+constexpr int kGemmMinTokens = 256;
+
+struct GemmArgs {
+    int32_t T, d, N, K, C, I, Is;
+    const uint16_t* x;
+    const int32_t* perm;
+    const int32_t* offsets;  // HIT class row of the bucket offsets
+    const int32_t* resident_slot;
+    const uint16_t* w13_pool;
+    const uint16_t* w2_pool;
+    const uint16_t* w13s;
+    const uint16_t* w2s;
+    uint16_t* h;
+    uint16_t* hs;
+    float* y_slots;
+    float* y_shared;
+    uint32_t* ctrl;
+};
+
+bool expert_gemm_applies(const FfnArgs& a);
+hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream_t s);
+
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);

@@ -14,6 +14,7 @@ Every arithmetic step runs inside libspice_moe (HIP kernels or its host path).
 """
 from __future__ import annotations
 
+import os
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
@@ -60,6 +61,25 @@ class HostLayer:
             self._lore[e] = synth.gen_lore(self.wl, self.layer, e)
         return self._lore[e]
 
+    def prefetch(self, experts: Sequence[int] = (), lore_experts: Sequence[int] = (), threads: int = 0) -> None:
+        """Draw the given experts' weights and LoRE factors on a thread pool (each draw has
+        its own seeded stream, so the result does not depend on the order)."""
+        from concurrent.futures import ThreadPoolExecutor
+
+        todo = [(0, e) for e in experts if e not in self._experts]
+        todo += [(1, e) for e in lore_experts if e not in self._lore]
+        if not todo:
+            return
+
+        def draw(item):
+            kind, e = item
+            return item, (synth.gen_expert if kind == 0 else synth.gen_lore)(self.wl, self.layer, e)
+
+        n = threads or min(16, os.cpu_count() or 1)
+        with ThreadPoolExecutor(n) as ex:
+            for (kind, e), v in ex.map(draw, todo):
+                (self._experts if kind == 0 else self._lore)[e] = v
+
     def resident_mask(self) -> np.ndarray:
         m = np.zeros(self.shape.n_experts, np.int32)
         m[self.resident] = 1
@@ -90,6 +110,8 @@ class DeviceLayer:
         self.w13s = to_tensor(host.w13s, dt, device)
         self.w2s = to_tensor(host.w2s, dt, device)
         slot = np.full(s.n_experts, -1, np.int32)
+        host.prefetch(range(s.n_experts) if host_exact else host.resident,
+                      range(s.n_experts) if s.lore_rank > 0 else ())
         self.w13_pool = torch.empty((max(self.C, 1), 2 * s.inter, s.d), dtype=td, device=device)
         self.w2_pool = torch.empty((max(self.C, 1), s.d, s.inter), dtype=td, device=device)
         for i, e in enumerate(host.resident):
