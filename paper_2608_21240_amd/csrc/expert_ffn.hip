@@ -348,9 +348,9 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
                     h.z = silu(sg.z) * su.z;
                     h.w = silu(sg.w) * su.w;
                     if (tile.kind == kKindHit)
-                        T_::store4(a.h, (size_t)(start + gi) * a.I + orow, h);
+                        T_::store4(a.h, (size_t)(start + gi) * a.ldh + orow, h);
                     else
-                        T_::store4(a.hs, (size_t)gi * a.Is + orow, h);
+                        T_::store4(a.hs, (size_t)gi * a.ldhs + orow, h);
                 }
             }
         }
@@ -465,9 +465,10 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
     for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
         const int hs0 = (tile.kind == kKindShared) ? 0 : start;
+        const size_t ld = (tile.kind == kKindShared) ? a.ldhs : a.ldh;
         const char* const hb[kTokTiles] = {
-            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + m, n - 1)) * kdim * es + kb,
-            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + 16 + m, n - 1)) * kdim * es + kb};
+            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + m, n - 1)) * ld * es + kb,
+            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + 16 + m, n - 1)) * ld * es + kb};
         const char* const a1[1] = {aw[0]};
         const char* const h1[1] = {hb[0]};
         if (nrt == 1) {

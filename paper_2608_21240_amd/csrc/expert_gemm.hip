@@ -5,15 +5,18 @@
 //   up   : H[pos][f] = silu(sum_k W1[f][k] x[k]) * (sum_k W3[f][k] x[k])   (bf16 out)
 //   down : Y[pos][j] = sum_k W2[j][k] H[pos][k]                            (fp32 out)
 //
-// Block tile: 128 weight rows x 128 tokens x 64 k, 4 waves of 64 x 64.  For `up`
-// the 128 weight rows are 64 W1 rows and the same 64 W3 rows, so each wave holds
-// the gate and up sums of its 32 features and applies SwiGLU in registers.  The
-// weight tile is the MFMA A operand and the token tile the B operand
-// (v_mfma_f32_16x16x32_bf16): a lane ends with 4 consecutive features of one
-// token, stored with one 8- (bf16) or 16-byte (fp32) write.
-// Both tiles are staged through LDS, double buffered, rows padded to 144 bytes so
-// that the 16 rows read by a fragment load land on disjoint bank groups.  Token
-// rows of an expert are gathered through perm once per tile.
+// Block tile: 256 weight rows x 256 tokens, 64 k per stage, 4 waves of 128 x 128
+// (the accumulators live in AGPRs; LDS traffic is 64 flop per byte read).
+// For `up` the 256 weight rows are 128 W1 rows and the same 128 W3 rows, so each
+// wave holds the gate and up sums of its 64 features and applies SwiGLU in
+// registers.  The weight tile is the MFMA A operand and the token tile the B
+// operand (v_mfma_f32_16x16x32_bf16): a lane ends with 4 consecutive features of
+// one token, stored with one 8- (bf16) or 16-byte (fp32) write.
+// Both tiles are staged through LDS (two stages, 128 KiB: one block per CU) in
+// 128-byte rows whose 16-byte chunks are XOR-swizzled by row (chunk c of row r at
+// c ^ ((r >> 1) & 7)), so fragment reads and staging writes are free of bank
+// conflicts.  Global loads for the next stage are issued before the MFMAs.  Token rows of an expert are
+// gathered through perm once per tile.
 // Tiles: the shared block first, then the HIT experts in id order; inside a group
 // the token tiles of one weight tile are consecutive (the weight tile is then
 // served from L2), and consecutive tiles are kept on one XCD.
@@ -26,16 +29,24 @@
 namespace spice {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kBM = 128;            // weight rows per tile
-constexpr int kBT = 128;            // tokens per tile
-constexpr int kBK = 64;             // contraction per stage
-constexpr int kRowBytes = kBK * 2;  // 128 bytes of a staged row
-constexpr int kLdsRow = kRowBytes + 16;
-constexpr int kTileLds = kBM * kLdsRow;       // one operand tile of one stage
-constexpr int kStageLds = 2 * kTileLds;       // weights + tokens
-constexpr int kChunks = kBM * kRowBytes / 16 / kThreads;  // 16-byte chunks per thread per operand tile
-static_assert(kBM == kBT, "both operand tiles are staged with one layout");
+constexpr int kWaveT = 64;                     // tokens per wave (a wave holds 128 features x kWaveT)
+constexpr int kThreads = 64 * 2 * (256 / kWaveT);  // 2 (features) x 256 / kWaveT (tokens) waves
+constexpr int kBM = 256;                       // weight rows per tile
+constexpr int kBT = 256;                       // tokens per tile
+constexpr int kBK = 64;                        // contraction per stage (32 or 64)
+constexpr int kWavesPerEU = kWaveT == 128 ? 1 : 2;  // waves per SIMD the register budget targets
+constexpr int kTS = kWaveT / 16;               // token sub-tiles per wave
+constexpr int kXcdBlocks = 32;                 // blocks one XCD runs at a time (32 CUs, 1 block each)
+constexpr int kRowBytes = kBK * 2;             // bytes of a staged row
+constexpr int kCPR = kBK / 8;                  // 16-byte chunks per staged row
+constexpr int kWTile = kBM * kRowBytes;        // weight tile of one stage
+constexpr int kStageLds = (kBM + kBT) * kRowBytes;
+constexpr int kRowStep = kThreads / kCPR;      // staging rows between a thread's chunks
+constexpr int kWChunks = kBM * kCPR / kThreads;  // 16-byte weight chunks per thread per stage
+constexpr int kXChunks = kBT * kCPR / kThreads;  // 16-byte token chunks per thread per stage
+constexpr int kUpFeat = kBM / 2;               // features of an up tile (W1 rows = W3 rows)
+constexpr int kPrefetch = 1;                   // stages of global loads in flight (1 or 2)
+static_assert(kBK == 32 || kBK == 64, "a stage is one or two MFMA k-steps");
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -49,18 +60,25 @@ __device__ __forceinline__ uint32_t bf16_rne(float f) {
 
 __device__ __forceinline__ float silu(float u) { return u / (1.0f + __expf(-u)); }
 
-// Logical tile of block b when the hardware deals blocks to the 8 XCDs round robin:
-// each XCD gets one contiguous range of logical tiles (a bijection on [0, G)).
+// Logical tile of block b.  The hardware deals blocks to the 8 XCDs round robin
+// (block b to XCD b % 8).  Here every round of 8 x 32 blocks gives each XCD 32
+// consecutive logical tiles (neighbouring tiles share operands in that XCD's L2),
+// and the rounds alternate over all XCDs so that long tiles at the front of the
+// order spread over the whole chip.  A final partial round keeps block order; the
+// map is a bijection on [0, G).
 __device__ __forceinline__ int xcd_tile(int b, int G) {
-    const int x = b & 7, per = G >> 3, rem = G & 7;
-    const int first = x < rem ? x * (per + 1) : rem * (per + 1) + (x - rem) * per;
-    return first + (b >> 3);
+    constexpr int kRound = 8 * kXcdBlocks;
+    if (b >= (G / kRound) * kRound) return b;
+    const int x = b & 7, slot = b >> 3;
+    return (slot / kXcdBlocks) * kRound + x * kXcdBlocks + slot % kXcdBlocks;
 }
 
 struct TileJob {
     const uint16_t* w;    // weight matrix of the group (rows of W13 or W2)
     const uint16_t* act;  // activations: x (up) or H / Hs (down)
     int kdim;             // contraction length
+    int ld;               // row stride (elements) of the activations inside one stage
+    uint32_t kst;         // elements between consecutive stages of one activation row
     int wrow0;            // first weight row of this tile (up: W1 row; W3 row = wrow0 + up_off)
     int up_off;           // up: row distance from W1 to W3 inside w
     int tok0, ntok;       // tile's first bucket position / token count of the group
@@ -74,16 +92,24 @@ struct TileJob {
 template <bool kUp>
 __device__ bool resolve(const GemmArgs& a, int L, TileJob& j, int* s_scan) {
     const int lane = threadIdx.x & 63;
-    const int nt_sh = kUp ? a.Is / 64 : a.d / kBM;  // weight tiles of the shared block
-    const int nt_e = kUp ? a.I / 64 : a.d / kBM;    // weight tiles of a routed expert
+    const int nt_sh = kUp ? a.Is / kUpFeat : a.d / kBM;  // weight tiles of the shared block
+    const int nt_e = kUp ? a.I / kUpFeat : a.d / kBM;    // weight tiles of a routed expert
     const int mt_sh = (a.T + kBT - 1) / kBT;
     const int tiles_sh = a.Is > 0 ? nt_sh * mt_sh : 0;
     if (L < tiles_sh) {
-        const int n = L / mt_sh, m = L - n * mt_sh;
+        // groups of sn weight tiles x sm token tiles (about one XCD's worth of blocks)
+        // run together and share their operand tiles in that XCD's L2
+        const int sn = kUp ? a.super_up[0] : a.super_dn[0], sm = kUp ? a.super_up[1] : a.super_dn[1];
+        const int g = L / (sn * sm), in = L - g * (sn * sm);
+        const int mg = mt_sh / sm;
+        const int n = (g / mg) * sn + in / sm;
+        const int m = (g % mg) * sm + in % sm;
         j.w = kUp ? a.w13s : a.w2s;
         j.act = kUp ? a.x : a.hs;
         j.kdim = kUp ? a.d : a.Is;
-        j.wrow0 = kUp ? n * 64 : n * kBM;
+        j.ld = kUp ? a.d : kBK;
+        j.kst = kUp ? kBK : (uint32_t)a.T * kBK;
+        j.wrow0 = kUp ? n * kUpFeat : n * kBM;
         j.up_off = a.Is;
         j.tok0 = m * kBT;
         j.ntok = a.T;
@@ -147,12 +173,16 @@ __device__ bool resolve(const GemmArgs& a, int L, TileJob& j, int* s_scan) {
         j.w = a.w13_pool + (size_t)slot * 2 * a.I * a.d;
         j.act = a.x;
         j.kdim = a.d;
-        j.wrow0 = nn * 64;
+        j.ld = a.d;
+        j.kst = kBK;
+        j.wrow0 = nn * kUpFeat;
         j.up_off = a.I;
     } else {
         j.w = a.w2_pool + (size_t)slot * a.d * a.I;
         j.act = a.h;
         j.kdim = a.I;
+        j.ld = kBK;
+        j.kst = (uint32_t)a.T * a.K * kBK;
         j.wrow0 = nn * kBM;
         j.up_off = 0;
     }
@@ -165,30 +195,44 @@ __device__ bool resolve(const GemmArgs& a, int L, TileJob& j, int* s_scan) {
     return true;
 }
 
+// Byte offset of 16-byte chunk c of staged row r inside an operand tile.
+// XOR swizzle of the 16-byte chunks of a staged row.  Measured on gfx950 with the
+// LDS bank-conflict counter: 128-byte rows swizzled by (r >> 1) & 7 read 16 rows x 4
+// chunks per ds_read_b128 and write 8 chunks per row without conflicts, where padded
+// rows, 64-byte rows and unswizzled rows do not.
+__device__ __forceinline__ uint32_t lds_off(int r, int c) {
+    const int sw = kBK == 64 ? ((r >> 1) & 7) : ((r >> 2) & 3);
+    return (uint32_t)(r * kRowBytes + ((c ^ sw) << 4));
+}
+
 template <bool kUp>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void expert_gemm_kernel(GemmArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWavesPerEU))) void expert_gemm_kernel(
+    GemmArgs a) {
     extern __shared__ __align__(16) unsigned char s_lds[];
     __shared__ int s_scan[4];
     TileJob j;
     if (!resolve<kUp>(a, xcd_tile(blockIdx.x, gridDim.x), j, s_scan)) return;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int wf = w & 1, wt = w >> 1;  // wave's feature half and token half of the tile
+    const int wf = w & 1, wt = w >> 1;  // wave's feature half and token block of the tile
     const int m = lane & 15, quad = lane >> 4;
 
-    // This thread's staging chunks: rows r_i = tid / 8 + 32 i, 16-byte column c = tid % 8.
-    const int c16 = tid & 7;
-    const uint16_t* wsrc[kChunks];
-    const uint16_t* xsrc[kChunks];
+    // Staging: this thread moves chunk c16 = tid % kCPR of rows r0 + kRowStep i.  Weight
+    // rows step by a constant, so one 32-bit element offset (from the group's uniform
+    // base pointer) and uniform deltas address them; token rows are gathered.
+    const int c16 = tid % kCPR, r0 = tid / kCPR;
+    static_assert(kRowStep % 16 == 0 && kUpFeat % kRowStep == 0, "staging rows keep their swizzle");
+    const uint32_t woff0 = (uint32_t)(j.wrow0 + r0) * (uint32_t)j.kdim + c16 * 8;
+    auto wrow_delta = [&](int i) -> uint32_t {  // rows between chunk 0 and chunk i (uniform)
+        const int r = kRowStep * i;
+        if (kUp && r >= kUpFeat) return (uint32_t)(j.up_off + r - kUpFeat) * (uint32_t)j.kdim;
+        return (uint32_t)r * (uint32_t)j.kdim;
+    };
+    uint32_t xoff[kXChunks];
 #pragma unroll
-    for (int i = 0; i < kChunks; ++i) {
-        const int r = (tid >> 3) + 32 * i;
-        int wr;
-        if (kUp) wr = r < 64 ? j.wrow0 + r : j.wrow0 + j.up_off + (r - 64);
-        else wr = j.wrow0 + r;
-        wsrc[i] = j.w + (size_t)wr * j.kdim + c16 * 8;
+    for (int i = 0; i < kXChunks; ++i) {
         // token rows past the group's end read its last row; their outputs are dropped
-        const int pos = min(j.tok0 + r, j.ntok - 1);
+        const int pos = min(j.tok0 + r0 + kRowStep * i, j.ntok - 1);
         int row;
         if (j.shared) {
             row = pos;
@@ -203,105 +247,161 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         } else {
             row = j.start + pos;
         }
-        xsrc[i] = j.act + (size_t)row * j.kdim + c16 * 8;
+        xoff[i] = (uint32_t)row * (uint32_t)j.ld + c16 * 8;
     }
+    const uint16_t* __restrict__ wbase = j.w;
+    const uint16_t* __restrict__ xbase = j.act;
 
-    f32x4_t acc[4][4];
+    f32x4_t acc[8][kTS];
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 8; ++s)
 #pragma unroll
-        for (int t = 0; t < 4; ++t) acc[s][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+        for (int t = 0; t < kTS; ++t) acc[s][t] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    u32x4_t wreg[kChunks], xreg[kChunks];
-    auto load_stage = [&](int kt) {
-        const size_t off = (size_t)kt * kBK;
-#pragma unroll
-        for (int i = 0; i < kChunks; ++i) {
-            wreg[i] = *reinterpret_cast<const u32x4_t*>(wsrc[i] + off);
-            xreg[i] = *reinterpret_cast<const u32x4_t*>(xsrc[i] + off);
-        }
-    };
-    auto store_stage = [&](int buf) {
-        unsigned char* wl = s_lds + buf * kStageLds;
-        unsigned char* xl = wl + kTileLds;
-#pragma unroll
-        for (int i = 0; i < kChunks; ++i) {
-            const int r = (tid >> 3) + 32 * i;
-            *reinterpret_cast<u32x4_t*>(wl + r * kLdsRow + c16 * 16) = wreg[i];
-            *reinterpret_cast<u32x4_t*>(xl + r * kLdsRow + c16 * 16) = xreg[i];
-        }
-    };
+    // LDS addresses.  The swizzle of row r depends on (r >> 1) & 7, which steps of 16
+    // rows leave unchanged, so every sub-tile / staging chunk is a constant offset from
+    // one base.  Fragments of k-step 0; with kBK = 64, k-step 1 reads chunk c ^ 4, i.e.
+    // the address with bit 6 flipped.  Weights (A): for `up` the wave's feature
+    // sub-tiles 0..3 are W1 rows wf*64 + 16 s and 4..7 the W3 rows kUpFeat + the same.
+    const uint32_t fbase = lds_off(kUp ? wf * 64 + m : wf * 128 + m, quad);
+    const uint32_t tbase = kWTile + lds_off(wt * kWaveT + m, quad);
+    const uint32_t sbase = lds_off(r0, c16);
+    auto frag_row = [](int s) { return kUp ? (s & 3) * 16 + (s >> 2) * kUpFeat : s * 16; };
 
-    // Fragment rows of this wave: weights (A) and tokens (B).  For `up` the wave's
-    // feature sub-tiles are W1 rows wf*32 + {0, 16} and the W3 rows 64 + the same.
-    int frow[4], trow[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        frow[s] = kUp ? ((s < 2 ? 0 : 64) + wf * 32 + (s & 1) * 16 + m) : (wf * 64 + s * 16 + m);
-        trow[s] = wt * 64 + s * 16 + m;
-    }
-
+    u32x4_t stg[kPrefetch][kWChunks + kXChunks];
     const int nk = j.kdim / kBK;
-    load_stage(0);
-    store_stage(0);
-    __syncthreads();
-    for (int kt = 0; kt < nk; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < nk) load_stage(kt + 1);
-        const unsigned char* wl = s_lds + buf * kStageLds;
-        const unsigned char* xl = wl + kTileLds;
+    auto load = [&](int set, int kt) {
+        const uint32_t o = (uint32_t)kt * kBK, ox = (uint32_t)kt * j.kst;
+#pragma unroll
+        for (int i = 0; i < kWChunks; ++i)
+            stg[set][i] = *reinterpret_cast<const u32x4_t*>(wbase + woff0 + wrow_delta(i) + o);
+#pragma unroll
+        for (int i = 0; i < kXChunks; ++i)
+            stg[set][kWChunks + i] = *reinterpret_cast<const u32x4_t*>(xbase + xoff[i] + ox);
+    };
+    auto store = [&](int set, int buf) {
+        unsigned char* base = s_lds + buf * kStageLds + sbase;
+#pragma unroll
+        for (int i = 0; i < kWChunks; ++i)
+            *reinterpret_cast<u32x4_t*>(base + i * kRowStep * kRowBytes) = stg[set][i];
+#pragma unroll
+        for (int i = 0; i < kXChunks; ++i)
+            *reinterpret_cast<u32x4_t*>(base + kWTile + i * kRowStep * kRowBytes) = stg[set][kWChunks + i];
+    };
+    auto compute = [&](int buf) {
+        const unsigned char* base = s_lds + buf * kStageLds;
 #pragma unroll
         for (int ks = 0; ks < kBK / 32; ++ks) {
-            const int kb = (ks * 32 + quad * 8) * 2;
-            u32x4_t af[4], bf[4];
+            const uint32_t kx = ks ? 64u : 0u;
+            // every fragment of the k-step is requested before the first MFMA, so the LDS
+            // latency is paid once per k-step rather than once per A fragment
+            u32x4_t bfr[kTS], afr[8];
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                af[s] = *reinterpret_cast<const u32x4_t*>(wl + frow[s] * kLdsRow + kb);
-                bf[s] = *reinterpret_cast<const u32x4_t*>(xl + trow[s] * kLdsRow + kb);
-            }
+            for (int t = 0; t < kTS; ++t)
+                bfr[t] = *reinterpret_cast<const u32x4_t*>(base + ((tbase + t * 16 * kRowBytes) ^ kx));
 #pragma unroll
-            for (int s = 0; s < 4; ++s)
+            for (int s = 0; s < 8; ++s)
+                afr[s] = *reinterpret_cast<const u32x4_t*>(base + ((fbase + frag_row(s) * kRowBytes) ^ kx));
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-                for (int t = 0; t < 4; ++t)
-                    acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[s]),
-                                                                        __builtin_bit_cast(bf16x8_t, bf[t]),
+            for (int s = 0; s < 8; ++s)
+#pragma unroll
+                for (int t = 0; t < kTS; ++t)
+                    acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, afr[s]),
+                                                                        __builtin_bit_cast(bf16x8_t, bfr[t]),
                                                                         acc[s][t], 0, 0, 0);
+            __builtin_amdgcn_sched_barrier(0);
         }
-        if (kt + 1 < nk) store_stage(buf ^ 1);
+    };
+
+    if constexpr (kPrefetch == 2) {
+        // stage k is computed from LDS buffer k % 2; its global loads were issued two
+        // iterations earlier into register set k % 2
+        load(0, 0);
+        if (nk > 1) load(1, 1);
+        store(0, 0);
         __syncthreads();
+        for (int kt = 0; kt < nk; kt += 2) {
+            if (kt + 2 < nk) load(0, kt + 2);
+            compute(0);
+            if (kt + 1 < nk) store(1, 1);
+            __syncthreads();
+            if (kt + 1 >= nk) break;
+            if (kt + 3 < nk) load(1, kt + 3);
+            compute(1);
+            if (kt + 2 < nk) store(0, 0);
+            __syncthreads();
+        }
+    } else {
+        load(0, 0);
+        store(0, 0);
+        __syncthreads();
+        for (int kt = 0; kt < nk; ++kt) {
+            if (kt + 1 < nk) load(0, kt + 1);
+            compute(kt & 1);
+            if (kt + 1 < nk) store(0, (kt + 1) & 1);
+            __syncthreads();
+        }
     }
 
     // Epilogue: lane holds features 4*quad .. +3 of sub-tile s for token m of sub-tile t.
 #pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        const int pos = j.tok0 + wt * 64 + t * 16 + m;
+    for (int t = 0; t < kTS; ++t) {
+        const int pos = j.tok0 + wt * kWaveT + t * 16 + m;
         if (pos >= j.ntok) continue;
         if (kUp) {
+            // intermediates are k-blocked: element (row, f) at ((f / kBK) * rows + row) * kBK + f % kBK,
+            // so a down-projection stage reads its token rows as one contiguous block
+            uint16_t* dst = j.shared ? a.hs + (size_t)pos * kBK : a.h + (size_t)(j.start + pos) * kBK;
+            const size_t fstride = (size_t)(j.shared ? a.T : a.T * a.K) * kBK;
 #pragma unroll
-            for (int s = 0; s < 2; ++s) {
-                const f32x4_t g = acc[s][t], u = acc[s + 2][t];
-                const int f = j.feat0 + wf * 32 + s * 16 + quad * 4;
+            for (int s = 0; s < 4; ++s) {
+                const f32x4_t g = acc[s][t], u = acc[s + 4][t];
+                const int f = j.feat0 + wf * 64 + s * 16 + quad * 4;
                 uint2 p;
                 p.x = bf16_rne(silu(g.x) * u.x) | (bf16_rne(silu(g.y) * u.y) << 16);
                 p.y = bf16_rne(silu(g.z) * u.z) | (bf16_rne(silu(g.w) * u.w) << 16);
-                uint16_t* dst = j.shared ? a.hs + (size_t)pos * a.Is : a.h + (size_t)(j.start + pos) * a.I;
-                *reinterpret_cast<uint2*>(dst + f) = p;
+                *reinterpret_cast<uint2*>(dst + (size_t)(f / kBK) * fstride + (f % kBK)) = p;
             }
         } else {
+            float* dst = j.shared ? a.y_shared + (size_t)pos * a.d : a.y_slots + (size_t)(j.start + pos) * a.d;
 #pragma unroll
-            for (int s = 0; s < 4; ++s) {
-                const int f = j.feat0 + wf * 64 + s * 16 + quad * 4;
-                float* dst = j.shared ? a.y_shared + (size_t)pos * a.d : a.y_slots + (size_t)(j.start + pos) * a.d;
+            for (int s = 0; s < 8; ++s) {
+                const int f = j.feat0 + wf * 128 + s * 16 + quad * 4;
                 *reinterpret_cast<f32x4_t*>(dst + f) = acc[s][t];
             }
         }
     }
 }
 
+// Super-tile of the shared block: sn weight tiles x sm token tiles with sn | nt and
+// sm | mt, at most one XCD round of blocks, as square as possible (the bytes a group
+// fetches per stage are proportional to sn + sm).
+void super_shape(int mt, int nt, int* out) {
+    int best_n = 1, best_m = 1, best_score = -1;
+    for (int sm = 1; sm <= mt && sm <= kXcdBlocks; ++sm) {
+        if (mt % sm) continue;
+        for (int sn = 1; sn <= nt && sn * sm <= kXcdBlocks; ++sn) {
+            if (nt % sn) continue;
+            // more blocks per group first, then fewer distinct tiles per block
+            const int score = sn * sm * 64 - (sn + sm);
+            if (score > best_score) { best_score = score; best_n = sn; best_m = sm; }
+        }
+    }
+    out[0] = best_n;
+    out[1] = best_m;
+}
+
 }  // namespace
 
 bool expert_gemm_applies(const FfnArgs& a) {
-    if (a.dtype != SPICE_BF16 || a.T < kGemmMinTokens || a.d % kBM || a.d % kBK || a.I % 64 || a.Is % 64)
+    if (a.dtype != SPICE_BF16 || a.T < kGemmMinTokens || a.d % kBM || a.d % kBK || a.I % kUpFeat ||
+        a.Is % kUpFeat || a.I % kBK || a.Is % kBK)
+        return false;
+    // element offsets inside one operand are 32-bit
+    const long long lim = 0x7FFFFFFFll;
+    if ((long long)a.I * a.T * a.K > lim || (long long)a.Is * a.T > lim || (long long)a.d * a.T * a.K > lim ||
+        2ll * a.I * a.d > lim || 2ll * a.Is * a.d > lim)
         return false;
     // the double-buffered tiles need more LDS than the 64 KiB every AMD GPU offers
     static int lds_per_block[64] = {0};
@@ -318,6 +418,7 @@ bool expert_gemm_applies(const FfnArgs& a) {
 hipError_t launch_expert_gemm(const FfnArgs& f, bool hit, bool shared, hipStream_t s) {
     GemmArgs a{};
     a.T = f.T; a.d = f.d; a.N = f.N; a.K = f.K; a.C = f.C; a.I = f.I; a.Is = shared ? f.Is : 0;
+    a.ldh = f.ldh; a.ldhs = f.ldhs;
     a.x = static_cast<const uint16_t*>(f.x);
     a.perm = f.perm;
     a.offsets = f.offsets;  // the HIT class comes first
@@ -335,10 +436,14 @@ hipError_t launch_expert_gemm(const FfnArgs& f, bool hit, bool shared, hipStream
     // upper bound of the tile count: sum_e ceil(n_e / kBT) <= T*K / kBT + min(N, C)
     const long long mt_hit = hit ? (long long)a.T * a.K / kBT + std::min(a.N, a.C) : 0;
     const long long mt_sh = (a.T + kBT - 1) / kBT;
-    const long long up_tiles = (a.Is > 0 ? mt_sh * (a.Is / 64) : 0) + mt_hit * (a.I / 64);
+    const long long up_tiles = (a.Is > 0 ? mt_sh * (a.Is / kUpFeat) : 0) + mt_hit * (a.I / kUpFeat);
     const long long dn_tiles = (a.Is > 0 ? mt_sh * (a.d / kBM) : 0) + mt_hit * (a.d / kBM);
     if (up_tiles == 0) return hipSuccess;
     if (up_tiles > 0x7FFFFFFFll || dn_tiles > 0x7FFFFFFFll) return hipErrorInvalidValue;
+    if (a.Is > 0) {
+        super_shape((int)mt_sh, a.Is / kUpFeat, a.super_up);
+        super_shape((int)mt_sh, a.d / kBM, a.super_dn);
+    }
     const size_t lds = 2 * kStageLds;
     hipLaunchKernelGGL(expert_gemm_kernel<true>, dim3((unsigned)up_tiles), dim3(kThreads), lds, s, a);
     hipError_t e = hipGetLastError();

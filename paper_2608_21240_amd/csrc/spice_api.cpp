@@ -122,8 +122,8 @@ WsLayout ws_layout(const spice_moe_cfg_t& c, int32_t T) {
     const size_t t = (size_t)std::max(T, 0), slots = t * (size_t)c.top_k, es = elem_size(c);
     size_t off = SPICE_WS_CONTROL_BYTES;
     L.logits = off; off += align256(t * (size_t)c.n_experts * sizeof(double));
-    L.h = off;      off += align256(slots * (size_t)c.inter * es);
-    L.hs = off;     off += align256(t * (size_t)c.shared_inter * es);
+    L.h = off;      off += align256(slots * ((size_t)c.inter + kHPad) * es);
+    L.hs = off;     off += align256(t * ((size_t)c.shared_inter + kHPad) * es);
     L.u = off;      off += align256(slots * (size_t)c.lore_rank * sizeof(float));
     L.total = off;
     return L;
@@ -265,6 +265,7 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
     spice::FfnArgs a{};
     a.T = T; a.d = c.d; a.N = c.n_experts; a.K = c.top_k; a.C = c.n_slots; a.I = c.inter;
     a.Is = c.shared_inter; a.r = c.lore_rank; a.dtype = c.dtype; a.groups = groups;
+    a.ldh = c.inter + spice::kHPad; a.ldhs = c.shared_inter + spice::kHPad;
     a.x = x; a.perm = perm; a.offsets = offsets; a.resident_slot = resident_slot;
     a.w13_pool = w13_pool; a.w2_pool = w2_pool; a.w13s = w13_shared; a.w2s = w2_shared;
     a.lore_A = lore_A; a.lore_B = lore_B; a.y_slots = y_slots; a.y_shared = y_shared;

@@ -26,11 +26,16 @@ inline int route_tokens_per_block(int d, int es) {
     return tt > kRouteTok ? kRouteTok : tt;
 }
 
+// Row padding (elements) of the SwiGLU intermediates in the workspace: row strides
+// that are multiples of large powers of two put every row of a tile on the same
+// HBM channel.
+constexpr int kHPad = 64;
+
 // Byte offsets of the workspace regions for one (cfg, T).
 struct WsLayout {
     size_t logits;  // fp64 [T][N]
-    size_t h;       // SwiGLU intermediate of routed slots [T*K][I] (dtype)
-    size_t hs;      // shared-block intermediate [T][I_s] (dtype)
+    size_t h;       // SwiGLU intermediate of routed slots [T*K][I + kHPad] (dtype)
+    size_t hs;      // shared-block intermediate [T][I_s + kHPad] (dtype)
     size_t u;       // LoRE A x, fp32 [T*K][r]
     size_t total;
 };
@@ -66,6 +71,7 @@ struct RouteArgs {
 
 struct FfnArgs {
     int32_t T, d, N, K, C, I, Is, r, dtype, groups;
+    int32_t ldh, ldhs;  // row strides (elements) of h and hs
     const void* x;
     const int32_t* perm;
     const int32_t* offsets;
@@ -101,6 +107,8 @@ constexpr int kGemmMinTokens = 256;
 
 struct GemmArgs {
     int32_t T, d, N, K, C, I, Is;
+    int32_t ldh, ldhs;
+    int32_t super_up[2], super_dn[2];  // shared-block super-tile (weight tiles, token tiles)
     const uint16_t* x;
     const int32_t* perm;
     const int32_t* offsets;  // HIT class row of the bucket offsets

@@ -1,7 +1,7 @@
 """GPU parity of the prefill path: at T >= 256 tokens (bf16, tile-aligned sizes) the
 HIT experts and the shared block run as grouped MFMA GEMMs.
 
-  - a reduced layer (d=256, N=16, K=4, I=192, I_s=320, r=16) at T=300 and 600, every
+  - a reduced layer (d=256, N=16, K=4, I=256, I_s=384, r=16) at T=300 and 600, every
     token against the oracle, all resident and partly resident (LoRE + exact misses),
     token tiles with ragged tails;
   - the Qwen2-57B-A14B-shaped prefill layer (T=4096, top-8, Zipf(1.1) routing skew),
@@ -17,7 +17,7 @@ from parity import EXACT, HIT, LORE, Case, say
 
 pytestmark = pytest.mark.gpu
 
-PF_SMALL = W.MoEShape(d=256, n_experts=16, top_k=4, inter=192, shared_inter=320, lore_rank=16, dtype=W.DTYPE_BF16)
+PF_SMALL = W.MoEShape(d=256, n_experts=16, top_k=4, inter=256, shared_inter=384, lore_rank=16, dtype=W.DTYPE_BF16)
 
 
 @pytest.mark.parametrize("T,R", [(300, 16), (300, 8), (600, 5)])
