@@ -42,9 +42,9 @@ METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shap
 # one the counters were taken on.
 TRAFFIC_RECORD = {
     "kernel_source": "paper_2608_21240_amd/csrc/expert_ffn.hip",
-    "source_sha256_16": "bbb39a0f198b7fae",
-    "fetch_kib_per_call": 189670 + 98806,
-    "write_kib_per_call": 463 + 1451,
+    "source_sha256_16": "46f66a1643356acf",
+    "fetch_kib_per_call": 189696.4 + 98684.14,
+    "write_kib_per_call": 462.98 + 1450.9,
     "fetch_factor": 2.0,
     "write_factor": 1.0,
     "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
@@ -63,6 +63,10 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="finish with a plain device copy of this many MiB (a known-size reference for counters)")
+    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill"),
+                   help="dsv2_decode: the decode layer (default); qwen2_prefill: the 4096-token "
+                        "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path")
+    p.add_argument("--resident", type=int, default=64, help="qwen2_prefill: resident experts")
     return p.parse_args()
 
 
@@ -110,6 +114,8 @@ def main():
     from paper_2608_21240_amd import layer as LY, synth, workloads as W
 
     torch.cuda.set_device(0)
+    if args.workload == "qwen2_prefill":
+        return prefill_main(args)
     batches = [int(b) for b in args.batches.split(",")]
     wl = W.WORKLOADS["dsv2_decode_t32"]
     shape = wl.shape
@@ -208,6 +214,68 @@ def main():
         a = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         torch.empty_like(a).copy_(a)
         torch.cuda.synchronize()
+    print(json.dumps(line), flush=True)
+
+
+MFMA_BF16_PEAK_TFLOPS = 2500.0
+
+
+def prefill_main(args):
+    """Qwen2-57B-A14B-shaped layer at 4096 tokens: every step is a whole layer call
+    (route, grouped MFMA GEMMs of the HIT experts and the shared block, LoRE and the
+    exact CPU path for absent experts, combine); the roofline is MFMA-bound."""
+    import torch
+
+    from paper_2608_21240_amd import layer as LY, synth, workloads as W
+
+    wl = W.WORKLOADS["qwen2_prefill"].with_(resident=args.resident)
+    s, T = wl.shape, wl.tokens
+    t_gen = time.time()
+    host = LY.HostLayer(wl, 0)
+    dev = LY.DeviceLayer(host, host_exact=args.resident < s.n_experts)
+    run = LY.LayerRun(s, T, dev.C, tau=wl.tau)
+    x = LY.to_tensor(synth.gen_x(wl, 0, 0, T), s.dtype, "cuda")
+    conf = torch.from_numpy(synth.gen_conf(wl, 0, 0, T)).cuda()
+    exact = args.resident < s.n_experts
+    run.forward(dev, x, conf, T, exact=exact, n_threads=args.threads)
+    torch.cuda.synchronize()
+    cls = run.slot_class[:T].cpu().numpy()
+    n_hit, n_lore = int((cls == 0).sum()), int((cls == 1).sum())
+    # FLOPs of the grouped FFN launch: SwiGLU of every HIT slot and of the shared block for
+    # every token (6 d I per token-expert pair), LoRE A and B products (4 d r per slot)
+    flops = 6.0 * T * s.d * s.shared_inter + 6.0 * n_hit * s.d * s.inter + 4.0 * n_lore * s.d * s.lore_rank
+    print(f"[bench] prefill layer ready in {time.time() - t_gen:.1f}s, classes "
+          f"{np.bincount(cls.ravel(), minlength=3).tolist()}", file=sys.stderr, flush=True)
+    for _ in range(args.warmup):
+        run.forward(dev, x, conf, T, exact=exact, n_threads=args.threads)
+    torch.cuda.synchronize()
+    names = ("start", "routed", "ffn0", "experts", "resid", "end")
+    evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        run.forward(dev, x, conf, T, exact=exact, n_threads=args.threads, events=evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    if run.flags() != 0:
+        raise RuntimeError("device flags raised")
+    ffn_ms = np.array([e["ffn0"].elapsed_time(e["experts"]) for e in evs])
+    achieved = flops / (ffn_ms.mean() * 1e-3) / 1e12
+    line = {
+        "metric": "MoE-layer prefill tokens/s + grouped-FFN MFMA TFLOP/s (% peak), Qwen2-57B-A14B-shaped",
+        "value": round(T * args.steps / wall, 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(1e3 * wall / args.steps, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init Qwen2-57B-A14B-shaped layer, Zipf(1.1) routing skew)",
+        "config": {"workload": f"qwen2_57b_a14b_moe_layer_prefill_T{T}_R{args.resident}", "hidden": s.d,
+                   "experts": s.n_experts, "top_k": s.top_k, "inter": s.inter, "shared_inter": s.shared_inter,
+                   "lore_rank": s.lore_rank, "resident": args.resident, "tokens": T},
+        "roofline": {"bound": "mfma", "kernel": "grouped expert FFN call: expert_gemm_kernel up + down "
+                                                "(moe_expert_ffn_grouped, T >= 256)",
+                     "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                     "flop_per_launch": flops, "avg_launch_us": round(float(ffn_ms.mean() * 1e3), 1)},
+        "classes": np.bincount(cls.ravel(), minlength=3).tolist(),
+    }
     print(json.dumps(line), flush=True)
 
 
