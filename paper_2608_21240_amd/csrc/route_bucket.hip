@@ -32,6 +32,8 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kMaxKeys = 3 * SPICE_MAX_EXPERTS;
 constexpr int kKeysPerThread = (kMaxKeys + kThreads - 1) / kThreads;
 constexpr int kMaxRowChunks = 16;  // 16-byte chunks of a router row per lane (d*es <= 16 KiB)
+constexpr int kBatch = 8;          // 64-slot chunks whose keys are read per round trip when bucketing
+constexpr int kRouteFusedMaxTiles = 16;  // token tiles up to which the three steps share one launch
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t bits16) {
     return __uint_as_float(bits16 << 16);
@@ -191,9 +193,18 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
     __syncthreads();
     const int per = (S + kWaves - 1) / kWaves;
     const int lo = min(S, w * per), hi = min(S, lo + per);
-    for (int s = lo + lane; s < hi; s += 64) {
-        const int key = slot_key(a, s);
-        if (key >= 0) atomicAdd(&s_base[w * NK + key], 1);
+    // keys are read kBatch chunks of 64 at a time, so that one memory round trip
+    // serves kBatch chunks (large batches of tokens have thousands of slots)
+    for (int base = lo; base < hi; base += 64 * kBatch) {
+        int key[kBatch];
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u) {
+            const int s = base + 64 * u + lane;
+            key[u] = s < hi ? slot_key(a, s) : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kBatch; ++u)
+            if (key[u] >= 0) atomicAdd(&s_base[w * NK + key[u]], 1);
     }
     __syncthreads();
 
@@ -240,9 +251,17 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
     if (a.h_counts && tid < 3) a.h_counts[tid] = s_ccount[tid];
 
     const unsigned long long lt_mask = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
-    for (int base = lo; base < hi; base += 64) {
-        const int s = base + lane;
-        const int key = (s < hi) ? slot_key(a, s) : -1;
+    for (int base0 = lo; base0 < hi; base0 += 64 * kBatch) {
+      int keys[kBatch];
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {
+          const int s = base0 + 64 * u + lane;
+          keys[u] = s < hi ? slot_key(a, s) : -1;
+      }
+#pragma unroll
+      for (int u = 0; u < kBatch; ++u) {  // chunks in slot order: ranks stay stable
+        const int s = base0 + 64 * u + lane;
+        const int key = keys[u];
         const bool valid = key >= 0;
         unsigned long long match = __ballot(valid);
 #pragma unroll
@@ -262,10 +281,16 @@ __device__ void bucket_all(const RouteArgs& a, int* s_base, int* s_run, int* s_w
             }
             if ((match >> lane) == 1ull) s_run[w * NK + key] += __popcll(match);
         }
+      }
     }
 }
 
-template <int DT>
+// kFused: one launch, later steps run in the last block to arrive (small T);
+// kLogitsOnly: step 1 only (large T: steps 2 and 3 are launches of their own, so no
+// block pays a device-scope fence; thousands of such fences cost more than launches).
+enum : int { kFused = 0, kLogitsOnly = 1 };
+
+template <int DT, int kMode>
 __global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int tt_tok) {
     extern __shared__ __align__(16) unsigned char s_dyn[];
     __shared__ int s_wsum[kWaves];
@@ -335,12 +360,28 @@ __global__ __launch_bounds__(kThreads) void route_bucket_kernel(RouteArgs a, int
         }
     }
 
+    if (kMode == kLogitsOnly) return;
     // 2. the last expert group of this token tile runs the gating (one wave per token)
     if (!is_last_arrival(&a.ctrl[kWordTileCounters + blockIdx.y], gridDim.x, &s_flag)) return;
     for (int i = w; i < nt; i += kWaves) topk_one_token(a, t0 + i, lane);
 
     // 3. the last token tile buckets every slot
     if (!is_last_arrival(&a.ctrl[kWordRouteDone], gridDim.y, &s_flag)) return;
+    int* s_base = reinterpret_cast<int*>(s_dyn);
+    bucket_all(a, s_base, s_base + kWaves * kMaxKeys, s_wsum, s_ccount);
+}
+
+// Step 2 on its own: one wave per token.
+__global__ __launch_bounds__(kThreads) void route_topk_kernel(RouteArgs a) {
+    const int t = blockIdx.x * kWaves + (threadIdx.x >> 6);
+    if (t < a.T) topk_one_token(a, t, threadIdx.x & 63);
+}
+
+// Step 3 on its own: one block.
+__global__ __launch_bounds__(kThreads) void route_sort_kernel(RouteArgs a) {
+    extern __shared__ __align__(16) unsigned char s_dyn[];
+    __shared__ int s_wsum[kWaves];
+    __shared__ int s_ccount[3];
     int* s_base = reinterpret_cast<int*>(s_dyn);
     bucket_all(a, s_base, s_base + kWaves * kMaxKeys, s_wsum, s_ccount);
 }
@@ -354,10 +395,23 @@ hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
     const size_t bucket_lds = (size_t)2 * kWaves * kMaxKeys * sizeof(int);
     const size_t lds = x_lds > bucket_lds ? x_lds : bucket_lds;
     dim3 grid((a.N + kRouteExp - 1) / kRouteExp, (a.T + tt - 1) / tt);
+    if ((int)grid.y <= kRouteFusedMaxTiles) {
+        if (a.dtype == SPICE_BF16)
+            hipLaunchKernelGGL((route_bucket_kernel<SPICE_BF16, kFused>), grid, dim3(kThreads), lds, s, a, tt);
+        else
+            hipLaunchKernelGGL((route_bucket_kernel<SPICE_F32, kFused>), grid, dim3(kThreads), lds, s, a, tt);
+        return hipGetLastError();
+    }
     if (a.dtype == SPICE_BF16)
-        hipLaunchKernelGGL(route_bucket_kernel<SPICE_BF16>, grid, dim3(kThreads), lds, s, a, tt);
+        hipLaunchKernelGGL((route_bucket_kernel<SPICE_BF16, kLogitsOnly>), grid, dim3(kThreads), x_lds, s, a, tt);
     else
-        hipLaunchKernelGGL(route_bucket_kernel<SPICE_F32>, grid, dim3(kThreads), lds, s, a, tt);
+        hipLaunchKernelGGL((route_bucket_kernel<SPICE_F32, kLogitsOnly>), grid, dim3(kThreads), x_lds, s, a, tt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(route_topk_kernel, dim3((a.T + kWaves - 1) / kWaves), dim3(kThreads), 0, s, a);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(route_sort_kernel, dim3(1), dim3(kThreads), bucket_lds, s, a);
     return hipGetLastError();
 }
 
