@@ -38,13 +38,13 @@ METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shap
 # HBM traffic of one grouped-FFN call (up + down kernels) at the headline batch, from
 # two rocprofv3 --pmc passes over this script (FETCH_SIZE, then WRITE_SIZE; KiB per
 # dispatch) scaled by what the counters read for a plain 1 GiB device copy
-# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Reported only while the kernel source is the
-# one the counters were taken on.
+# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Reported only while the kernel sources (the
+# two files hashed together) are the ones the counters were taken on.
 TRAFFIC_RECORD = {
-    "kernel_source": "paper_2608_21240_amd/csrc/expert_ffn.hip",
-    "source_sha256_16": "46f66a1643356acf",
-    "fetch_kib_per_call": 189696.4 + 98684.14,
-    "write_kib_per_call": 462.98 + 1450.9,
+    "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
+    "source_sha256_16": "f195a53f2f16a29d",
+    "fetch_kib_per_call": 189703.28 + 98533.28,
+    "write_kib_per_call": 462.98 + 1450.89,
     "fetch_factor": 2.0,
     "write_factor": 1.0,
     "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
@@ -67,6 +67,10 @@ def parse():
                    help="dsv2_decode: the decode layer (default); qwen2_prefill: the 4096-token "
                         "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path")
     p.add_argument("--resident", type=int, default=64, help="qwen2_prefill: resident experts")
+    p.add_argument("--split", default="auto", choices=("auto", "off"),
+                   help="exact-miss split (Eq. 12): auto = calibrate the cost model on this host and let the "
+                        "planner fetch experts to the GPU when that beats all-CPU; off = all-CPU")
+    p.add_argument("--fetch-slots", type=int, default=8, help="fetch pool slots for the exact-miss split")
     return p.parse_args()
 
 
@@ -74,8 +78,10 @@ def recorded_traffic():
     """HBM bytes per grouped-FFN call from the counter record, or None if the kernel changed."""
     import hashlib
 
-    path = os.path.join(ROOT, TRAFFIC_RECORD["kernel_source"])
-    sha = hashlib.sha256(open(path, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for rel in TRAFFIC_RECORD["kernel_sources"]:
+        h.update(open(os.path.join(ROOT, rel), "rb").read())
+    sha = h.hexdigest()[:16]
     if sha != TRAFFIC_RECORD["source_sha256_16"]:
         return None
     return int(1024 * (TRAFFIC_RECORD["fetch_kib_per_call"] * TRAFFIC_RECORD["fetch_factor"]
@@ -130,8 +136,9 @@ def main():
           f"({devs[0].hbm_bytes() / 1e9:.2f} GB HBM each)", file=sys.stderr, flush=True)
 
     results = {}
+    split_info = {}
     for T in batches:
-        run = LY.LayerRun(shape, T, devs[0].C, tau=wl.tau)
+        run = LY.LayerRun(shape, T, devs[0].C, tau=wl.tau, fetch_slots=args.fetch_slots if args.split == "auto" else 0)
         xs = [LY.to_tensor(synth.gen_x(wl, i, 0, T), shape.dtype, "cuda") for i in range(args.instances)]
         confs = [torch.from_numpy(synth.gen_conf(wl, i, 0, T)).cuda() for i in range(args.instances)]
         # per-instance class counts (fixed inputs per instance) from one untimed call
@@ -147,6 +154,19 @@ def main():
         torch.cuda.synchronize()
         if run.flags() != 0:
             raise RuntimeError("device flags raised during warmup")
+        split = None
+        if args.split == "auto":
+            # the calibration reads the routing copies of one call on the instance it passes
+            run.forward(devs[0], xs[0], confs[0], T, n_threads=args.threads)
+            torch.cuda.synchronize()
+            split = calibrate_split(run, devs[0], shape, T, args)
+        if split is not None:
+            split_info[T] = {f: float(f"{getattr(split, f):.4g}") for f, _ in split._fields_}
+            for w in range(args.warmup):
+                i = w % args.instances
+                run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, split=split)
+            torch.cuda.synchronize()
+        fetched = []
 
         names = ("start", "routed", "ffn0", "experts", "resid", "end")
         evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
@@ -156,8 +176,9 @@ def main():
         for k in range(args.steps):
             i = k % args.instances
             h0 = time.perf_counter()
-            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, events=evs[k])
+            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, events=evs[k], split=split)
             host_s += time.perf_counter() - h0
+            fetched.append(len(run.last_fetch))
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
 
@@ -179,6 +200,7 @@ def main():
             combine_us=float(comb_ms.mean() * 1e3), wait_for_host_us=float(wait_ms.mean() * 1e3),
             ffn_GBps=float(ffn_bytes.sum() / (ffn_ms.sum() * 1e-3) / 1e9),
             ffn_bytes_per_launch=float(ffn_bytes.mean()),
+            fetched_experts_per_step=float(np.mean(fetched)),
             classes=per_inst[0]["slots"], hit_experts=[p["hit_experts"] for p in per_inst],
             lore_experts=[p["lore_experts"] for p in per_inst], exact_experts=[p["exact_experts"] for p in per_inst],
         )
@@ -207,6 +229,8 @@ def main():
                      "combine_us": round(head["combine_us"], 2)},
         "by_batch": {str(T): {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()}
                      for T, r in results.items()},
+        "exact_split": {"mode": args.split, "fetch_slots": args.fetch_slots if args.split == "auto" else 0,
+                        "cost_model_by_batch": {str(T): c for T, c in split_info.items()}},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl.with_(tokens=head["T"]), hosts[0], args.cpu_baseline_seconds)
@@ -215,6 +239,64 @@ def main():
         torch.empty_like(a).copy_(a)
         torch.cuda.synchronize()
     print(json.dumps(line), flush=True)
+
+
+def calibrate_split(run, dev, shape, T, args):
+    """Cost model of the exact-miss split measured on this host, from the routing copies
+    of the last call on `dev`.
+
+    CPU: two timed residual calls over the same exact-miss experts, one with every exact
+    slot and one with only each expert's first slot (the other slots masked out), give the
+    rate over expert weights and the arithmetic rate per token (best of two each).
+    PCIe: one untimed fetch, then the best of two timed fetches into the pool."""
+    import torch
+
+    from paper_2608_21240_amd import spice
+
+    idx = run.idx_host[:T].numpy()
+    cls_all = run.cls_host[:T].numpy().copy()
+    exact = sorted(set(idx[cls_all == 2].tolist()))
+    if not exact:
+        return None
+    first = np.full(cls_all.shape, 1, np.uint8)  # LoRE slots are not the host's work
+    seen = set()
+    for t, k in zip(*np.nonzero(cls_all == 2)):
+        if idx[t, k] not in seen:
+            seen.add(idx[t, k])
+            first[t, k] = 2
+
+    def cpu_time(cls):
+        run.cls_host[:T].copy_(torch.from_numpy(cls))
+        best = float("inf")
+        for _ in range(2):
+            t0 = time.perf_counter()
+            spice.moe_exact_residual_host(run.cfg, T, run.x_host, run.idx_host, run.w_host, run.cls_host,
+                                          dev.host_w13, dev.host_w2, run.resid, args.threads)
+            best = min(best, time.perf_counter() - t0)
+        return best
+
+    t_all, t_first = cpu_time(cls_all), cpu_time(first)
+    run.cls_host[:T].copy_(torch.from_numpy(cls_all))
+    n_slots, n_exp = int((cls_all == 2).sum()), len(exact)
+    flops_tok = 6.0 * shape.inter * shape.d
+    extra = t_all - t_first
+    cpu_flops = (n_slots - n_exp) * flops_tok / extra if n_slots > n_exp and extra > 0 else 1e18
+    cpu_bytes = n_exp * shape.expert_bytes / max(t_first - n_exp * flops_tok / cpu_flops, 1e-9)
+    probe = [e for e in range(shape.n_experts) if dev.host_w13[e] is not None][: min(4, run.fetch_slots)]
+
+    def fetch_time():
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        with torch.cuda.stream(run.copy_stream):
+            spice.moe_fetch_experts(run.cfg, probe, dev.host_w13, dev.host_w2, run.w13_fetch, run.w2_fetch,
+                                    run.fetch_slots, run.fetch_expert, run.fetch_stage)
+        run.copy_stream.synchronize()
+        return time.perf_counter() - t0
+
+    fetch_time()
+    pcie = len(probe) * shape.expert_bytes / min(fetch_time(), fetch_time())
+    # the GPU side pays one fetched-FFN call (two launches); a split must save 5 %
+    return spice.spice_split_cost_t(cpu_bytes, cpu_flops, pcie, 30e-6, 0.05)
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0

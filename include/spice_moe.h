@@ -58,8 +58,11 @@ enum { SPICE_F32 = 0, SPICE_BF16 = 1 };
  * the caller's array, the slot's gate score, or the gate renormalised over the K. */
 enum { SPICE_CONF_INPUT = 0, SPICE_CONF_GATE = 1, SPICE_CONF_GATE_RENORM = 2 };
 /* Slot classes (Sec. 4.2): resident or prefetched -> exact on the GPU; missing with
- * confidence < tau -> shared + LoRE; otherwise an exact miss served on the CPU. */
-enum { SPICE_CLASS_HIT = 0, SPICE_CLASS_LORE = 1, SPICE_CLASS_EXACT = 2 };
+ * confidence < tau -> shared + LoRE; otherwise an exact miss served on the CPU.
+ * SPICE_CLASS_EXACT_GPU marks an exact miss whose expert was fetched for this call and
+ * computed on the GPU (M_fetch of Eq. 12); routing never produces it: moe_split_plan
+ * (host copy) and moe_expert_ffn_fetched (device copy) relabel EXACT slots to it. */
+enum { SPICE_CLASS_HIT = 0, SPICE_CLASS_LORE = 1, SPICE_CLASS_EXACT = 2, SPICE_CLASS_EXACT_GPU = 3 };
 
 #define SPICE_MAX_EXPERTS 256
 #define SPICE_MAX_TOKENS 65536
@@ -182,7 +185,7 @@ spice_status_t lore_surrogate_apply(const spice_moe_cfg_t* cfg, int32_t T, const
                                     void* ws, size_t ws_bytes, spice_stream_t stream);
 
 /*
- * Step 6: out[t] = (1 + sum_{k in LORE(t)} g) S(x_t) + sum_{k in HIT(t)} g y
+ * Step 6: out[t] = (1 + sum_{k in LORE(t)} g) S(x_t) + sum_{k in HIT(t) or EXACT_GPU(t)} g y
  *                  + sum_{k in LORE(t)} g delta + resid[t]
  * i.e. the gate-weighted sum of Sec. 2.1 with each LoRE slot's output replaced by
  * S(x) + B_e A_e x (Eq. 11) and the CPU outputs merged in (Sec. 4.3).
@@ -204,7 +207,7 @@ spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* t
  * threads (<= 0: one per online CPU).  The result does not depend on n_threads.
  *   x_host        host [T][d] (dtype)
  *   topk_idx_host host [T][K] int32, topk_w_host host [T][K] fp32,
- *   slot_class_host host [T][K] uint8
+ *   slot_class_host host [T][K] uint8 (only EXACT slots are computed; EXACT_GPU is skipped)
  *   w13_host      host table [N] of pointers to [2I][d] (dtype); entries of experts with
  *                 no EXACT slot may be NULL
  *   w2_host       host table [N] of pointers to [d][I] (dtype)
@@ -287,6 +290,67 @@ spice_status_t moe_cache_state(const spice_cache_t* cache, int32_t layer, int32_
 
 /* Wait for outstanding copies and free the handle (NULL is ignored). */
 void moe_cache_destroy(spice_cache_t* cache);
+
+/*
+ * Exact-miss split M = M_fetch + M_cpu (Eq. 12; Sec. 4.3).  The paper's scheduler serves
+ * every exact miss on the CPU unless fetching some of them over PCIe and running them
+ * on the GPU, in parallel with the CPU, beats that plan by a safety margin.  It gives no
+ * formula; this cost model is the library's own:
+ *   CPU time of a set   = sum_e (expert_bytes / cpu_bytes_per_s + n_e * flops / cpu_flops_per_s)
+ *   fetch time of a set = sum_e expert_bytes / pcie_bytes_per_s + gpu_fixed_s
+ *   plan time           = max(CPU time of M_cpu, fetch time of M_fetch)
+ * Candidates are taken in order of decreasing CPU cost (more tokens first, then lower
+ * id); the plan with the smallest time is kept if it is below (1 - margin) times the
+ * all-CPU time, otherwise nothing is fetched.
+ */
+typedef struct {
+    double cpu_bytes_per_s;   /* host DRAM rate of the exact CPU path over expert weights */
+    double cpu_flops_per_s;   /* its arithmetic rate (2 flops per multiply-add) */
+    double pcie_bytes_per_s;  /* host -> GPU copy rate */
+    double gpu_fixed_s;       /* fixed GPU-side cost of serving fetched experts (launches, FFN) */
+    double margin;            /* fraction the split must save over all-CPU, e.g. 0.05 */
+} spice_split_cost_t;
+
+/*
+ * Choose M_fetch from one call's routing (host copies, e.g. moe_route_bucket's host_out).
+ *   slot_class_host host [T][K] in/out: EXACT slots of the chosen experts become EXACT_GPU
+ *                   (so moe_exact_residual_host skips them)
+ *   max_fetch       most experts to fetch (the fetch pool's slots)
+ *   fetch_experts   host [max_fetch] out: chosen experts in order; n_fetch out: their count
+ */
+spice_status_t moe_split_plan(const spice_moe_cfg_t* cfg, int32_t T, const int32_t* topk_idx_host,
+                              uint8_t* slot_class_host, const spice_split_cost_t* cost, int32_t max_fetch,
+                              int32_t* fetch_experts, int32_t* n_fetch);
+
+/*
+ * Copy the chosen experts into a fetch pool on `copy_stream`: expert experts[i] into
+ * slot i of w13_fetch [n_slots][2I][d] / w2_fetch [n_slots][d][I], and write
+ * fetch_expert (device [n_slots] int32: expert id of each slot, -1 = unused) from the
+ * caller's pinned staging row fetch_expert_stage (host [n_slots]).  The caller orders
+ * its compute stream after `copy_stream` (an event) before moe_expert_ffn_fetched, and
+ * leaves fetch_expert_stage and the pools alone until `copy_stream` has passed the call.
+ *   w13_host, w2_host host tables [N] as in moe_exact_residual_host (pinned memory lets
+ *                     the copies run asynchronously)
+ */
+spice_status_t moe_fetch_experts(const spice_moe_cfg_t* cfg, int32_t n_fetch, const int32_t* experts,
+                                 const void* const* w13_host, const void* const* w2_host, void* w13_fetch,
+                                 void* w2_fetch, int32_t n_slots, int32_t* fetch_expert,
+                                 int32_t* fetch_expert_stage, spice_stream_t copy_stream);
+
+/*
+ * SwiGLU FFN (Eq. 6) of the fetched experts' EXACT slots on the GPU: for fetch slot j
+ * with expert e = fetch_expert[j] >= 0, every slot of the bucket (EXACT, e) gets its
+ * expert output in y_slots (row = bucket position) and its class becomes EXACT_GPU in
+ * slot_class, so moe_combine adds it like a HIT slot.
+ *   x, perm, offsets, slot_class  device, from moe_route_bucket (slot_class in/out)
+ *   fetch_expert  device [n_slots] int32, from moe_fetch_experts
+ *   w13_fetch, w2_fetch  device fetch pool
+ *   y_slots       device [T*K][d] fp32 out (those rows only)
+ */
+spice_status_t moe_expert_ffn_fetched(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
+                                      const int32_t* offsets, uint8_t* slot_class, const int32_t* fetch_expert,
+                                      const void* w13_fetch, const void* w2_fetch, int32_t n_slots,
+                                      float* y_slots, void* ws, size_t ws_bytes, spice_stream_t stream);
 
 /* Text of a status code, and the last error message of the calling thread. */
 const char* spice_status_string(spice_status_t status);

@@ -206,7 +206,7 @@ spice_status_t moe_cache_step(spice_cache_t* c, int32_t layer, int32_t step, int
         for (size_t i = 0; i < slots; ++i) {
             if (topk_idx_host[i] < 0 || topk_idx_host[i] >= N)
                 return err(SPICE_ERR_INVALID, "moe_cache_step: expert id out of range");
-            if (slot_class_host[i] > SPICE_CLASS_EXACT)
+            if (slot_class_host[i] > SPICE_CLASS_EXACT_GPU)
                 return err(SPICE_ERR_INVALID, "moe_cache_step: slot class out of range");
         }
         int32_t* se = &c->slot_expert[(size_t)layer * C];
@@ -215,8 +215,9 @@ spice_status_t moe_cache_step(spice_cache_t* c, int32_t layer, int32_t step, int
         for (int32_t s = 0; s < C; ++s)
             if (se[s] >= 0) where[se[s]] = s;
 
-        for (size_t i = 0; i < slots; ++i)
-            if (slot_class_host[i] == SPICE_CLASS_EXACT) ++wanted[topk_idx_host[i]];
+        for (size_t i = 0; i < slots; ++i)  // an exact miss served on the GPU is still a miss
+            if (slot_class_host[i] == SPICE_CLASS_EXACT || slot_class_host[i] == SPICE_CLASS_EXACT_GPU)
+                ++wanted[topk_idx_host[i]];
         if (c->device)
             for (int32_t e = 0; e < N; ++e)
                 if (wanted[e] > 0 && where[e] < 0 &&

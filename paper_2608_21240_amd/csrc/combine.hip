@@ -2,7 +2,7 @@
 // of the CPU exact residual (Sec. 4.3), plus a small fill kernel.
 //
 // One thread per 4 consecutive hidden features of one token; grid (d/1024, T).
-// out = (1 + sum_{LORE} g) * S(x) + sum_{HIT,LORE} g * y_slots[inv_perm[slot]] + resid.
+// out = (1 + sum_{LORE} g) * S(x) + sum_{HIT,LORE,EXACT_GPU} g * y_slots[inv_perm[slot]] + resid.
 #include <hip/hip_runtime.h>
 
 #include "spice_internal.h"
@@ -30,7 +30,7 @@ __global__ __launch_bounds__(256) void combine_kernel(CombineArgs a) {
     for (int k = 0; k < a.K; ++k) {
         const int s = t * a.K + k;
         const uint8_t c = a.slot_class[s];
-        if (c != SPICE_CLASS_HIT && c != SPICE_CLASS_LORE) continue;
+        if (c != SPICE_CLASS_HIT && c != SPICE_CLASS_LORE && c != SPICE_CLASS_EXACT_GPU) continue;
         const int pos = a.inv_perm[s];
         if (pos < 0 || pos >= S) continue;
         const float g = a.topk_w[s];

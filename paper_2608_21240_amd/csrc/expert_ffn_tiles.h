@@ -1,0 +1,479 @@
+// Tile code of the grouped expert FFN shared by its kernels (expert_ffn.hip: the
+// grouped HIT / shared / LoRE launches; expert_ffn_fetched.hip: the fetched-expert
+// launches).  Everything here has internal linkage: each kernel source compiles its
+// own copy, so a kernel added in one source leaves the other's code untouched.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "spice_internal.h"
+
+namespace spice {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = 4;
+constexpr int kTokTiles = 2;        // token tiles of 16 per pass
+constexpr int kDownRows = 2;        // 16-row tiles per down tile of a routed expert
+constexpr int kLoreRows = 256;      // B_e rows per LoRE tile (one per thread)
+constexpr int kLoreTok = 16;        // tokens per LoRE pass
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+template <int DT>
+struct Tr;
+
+template <>
+struct Tr<SPICE_BF16> {
+    static constexpr int kStep = 32;  // contraction elements per MFMA step
+    static constexpr int kLaneK = 8;  // elements each lane loads per step (16 bytes)
+    __device__ __forceinline__ static u32x4_t load(const void* base, size_t elem) {
+        return *reinterpret_cast<const u32x4_t*>(static_cast<const uint16_t*>(base) + elem);
+    }
+    __device__ __forceinline__ static f32x4_t mma(u32x4_t a, u32x4_t b, f32x4_t c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                       __builtin_bit_cast(bf16x8_t, b), c, 0, 0, 0);
+    }
+    // store 4 consecutive values of a row of the intermediate (bf16, round to nearest even)
+    __device__ __forceinline__ static void store4(void* base, size_t elem, f32x4_t v);
+};
+
+template <>
+struct Tr<SPICE_F32> {
+    static constexpr int kStep = 16;
+    static constexpr int kLaneK = 4;
+    __device__ __forceinline__ static u32x4_t load(const void* base, size_t elem) {
+        return *reinterpret_cast<const u32x4_t*>(static_cast<const float*>(base) + elem);
+    }
+    // four 16x16x4 steps; step j uses element j of every lane's 4-element chunk
+    __device__ __forceinline__ static f32x4_t mma(u32x4_t a, u32x4_t b, f32x4_t c) {
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+        return c;
+    }
+    __device__ __forceinline__ static void store4(void* base, size_t elem, f32x4_t v) {
+        *reinterpret_cast<f32x4_t*>(static_cast<float*>(base) + elem) = v;
+    }
+};
+
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return 0x7FC0u;  // NaN stays NaN
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+__device__ __forceinline__ void Tr<SPICE_BF16>::store4(void* base, size_t elem, f32x4_t v) {
+    uint2 p;
+    p.x = f32_to_bf16_rne(v.x) | (f32_to_bf16_rne(v.y) << 16);
+    p.y = f32_to_bf16_rne(v.z) | (f32_to_bf16_rne(v.w) << 16);
+    *reinterpret_cast<uint2*>(static_cast<uint16_t*>(base) + elem) = p;
+}
+
+__device__ __forceinline__ float silu(float u) { return u / (1.0f + __expf(-u)); }
+
+struct Group {
+    int e, start, n, slot;
+};
+
+// The j-th expert (ascending id) whose bucket of class c is non-empty; for HIT
+// buckets its pool slot is fetched in the same round trip as the offsets.
+__device__ bool find_group(const FfnArgs& a, int c, int j, Group& g) {
+    const int lane = threadIdx.x & 63;
+    const int32_t* off = a.offsets + c * (a.N + 1);
+    const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    int seen = 0;
+    for (int base = 0; base < a.N; base += 64) {
+        const int e = base + lane;
+        int st = 0, n = 0, slot = -1;
+        if (e < a.N) {
+            st = off[e];
+            n = off[e + 1] - st;
+            if (c == SPICE_CLASS_HIT) slot = a.resident_slot[e];
+        }
+        const unsigned long long m = __ballot(n > 0);
+        const int cnt = __popcll(m);
+        if (j < seen + cnt) {
+            const bool mine = n > 0 && __popcll(m & lt) == j - seen;
+            const int src = __ffsll((long long)__ballot(mine)) - 1;
+            g.e = base + src;
+            g.start = __shfl(st, src);
+            g.n = __shfl(n, src);
+            g.slot = __shfl(slot, src);
+            if (g.start < 0 || g.n < 0 || g.start + g.n > a.T * a.K) {
+                if (lane == 0) atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+                return false;
+            }
+            if (c == SPICE_CLASS_HIT && (g.slot < 0 || g.slot >= a.C)) {
+                if (lane == 0) atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_SLOT);
+                return false;
+            }
+            return true;
+        }
+        seen += cnt;
+    }
+    return false;
+}
+
+// Token of bucket position pos (0, flagged, if perm holds garbage).
+__device__ __forceinline__ int token_of(const FfnArgs& a, int pos) {
+    const int s = a.perm[pos];
+    if (s < 0 || s >= a.T * a.K) {
+        atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+        return 0;
+    }
+    return s / a.K;
+}
+
+enum : int { kKindHit = 0, kKindShared = 1, kKindLore = 2 };
+
+struct Tile {
+    int kind, ordinal, rt;
+};
+
+// Block index -> tile.  Segments: HIT experts x row tiles, shared-block row tiles,
+// LORE experts x row tiles (expert counts are upper bounds; surplus blocks exit).
+struct Grid {
+    int nhit, thit, tsh, nlore, tlore;
+    __device__ bool decode(int b, Tile& t) const {
+        if (b < nhit * thit) { t = {kKindHit, b / thit, b % thit}; return true; }
+        b -= nhit * thit;
+        if (b < tsh) { t = {kKindShared, 0, b}; return true; }
+        b -= tsh;
+        if (b < nlore * tlore) { t = {kKindLore, b / tlore, b % tlore}; return true; }
+        return false;
+    }
+};
+
+// ---------------------------------------------------------------------------
+// MFMA main loop shared by both launches.
+//   a[i]: per-lane pointer to weight row (tile row m = lane & 15) at the lane's k offset
+//   b[j]: per-lane pointer to the token row (column m) at the lane's k offset
+// Contraction steps [ks0, ks1) are all full (every lane's 16-byte chunk in range).
+// Loads of U steps are issued before their MFMAs so that many bytes are in flight.
+// ---------------------------------------------------------------------------
+constexpr int kStepBytes = 64;  // 32 bf16 or 16 fp32 per step per 4 lanes; same byte stride
+
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_steps(const char* const (&a)[NA], const char* const (&b)[NB], int ks0, int ks1,
+                                          f32x4_t (&acc)[NA][NB]) {
+    constexpr int U = (NA + NB <= 3) ? 8 : 4;
+    using T_ = Tr<DT>;
+    int ks = ks0;
+    for (; ks + U <= ks1; ks += U) {
+        u32x4_t av[NA][U], bv[NB][U];
+        const size_t off = (size_t)ks * kStepBytes;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+#pragma unroll
+            for (int i = 0; i < NA; ++i) av[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off + u * kStepBytes);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) bv[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off + u * kStepBytes);
+        }
+        __builtin_amdgcn_sched_barrier(0);  // keep every load of the group ahead of its MFMAs
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < NB; ++j)
+#pragma unroll
+                for (int i = 0; i < NA; ++i) acc[i][j] = T_::mma(av[i][u], bv[j][u], acc[i][j]);
+    }
+    const int rem = ks1 - ks;  // 0 .. U-1 steps left: one more group, loads clamped to the last step
+    if (rem > 0) {
+        u32x4_t av[NA][U], bv[NB][U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const size_t off = (size_t)(ks + min(u, rem - 1)) * kStepBytes;
+#pragma unroll
+            for (int i = 0; i < NA; ++i) av[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off);
+#pragma unroll
+            for (int j = 0; j < NB; ++j) bv[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (u < rem) {  // uniform across the wave
+#pragma unroll
+                for (int j = 0; j < NB; ++j)
+#pragma unroll
+                    for (int i = 0; i < NA; ++i) acc[i][j] = T_::mma(av[i][u], bv[j][u], acc[i][j]);
+            }
+        }
+    }
+}
+
+// The one partial contraction step (kdim not a multiple of the step): lanes whose
+// 16-byte chunk lies beyond kdim contribute zero.
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_tail(const char* const (&a)[NA], const char* const (&b)[NB], int ks, bool lane_in,
+                                         f32x4_t (&acc)[NA][NB]) {
+    const size_t off = (size_t)ks * kStepBytes;
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
+    u32x4_t av[NA], bv[NB];
+#pragma unroll
+    for (int i = 0; i < NA; ++i) av[i] = lane_in ? *reinterpret_cast<const u32x4_t*>(a[i] + off) : zero;
+#pragma unroll
+    for (int j = 0; j < NB; ++j) bv[j] = lane_in ? *reinterpret_cast<const u32x4_t*>(b[j] + off) : zero;
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+        for (int i = 0; i < NA; ++i) acc[i][j] = Tr<DT>::mma(av[i], bv[j], acc[i][j]);
+}
+
+// One wave's share of a (NA row streams) x (NB token tiles) product over kdim.
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void wave_product(const char* const (&a)[NA], const char* const (&b)[NB], int kdim, int w,
+                                             int quad, f32x4_t (&acc)[NA][NB]) {
+    constexpr int kStep = Tr<DT>::kStep;
+#pragma unroll
+    for (int i = 0; i < NA; ++i)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const int nfull = kdim / kStep;
+    const int nks = (kdim + kStep - 1) / kStep;
+    const int ks0 = w * nks / kWaves, ks1 = (w + 1) * nks / kWaves;
+    mma_steps<DT, NA, NB>(a, b, ks0, min(ks1, nfull), acc);
+    if (ks1 > nfull && nfull >= ks0)  // this wave owns the partial step
+        mma_tail<DT, NA, NB>(a, b, nfull, nfull * kStep + quad * Tr<DT>::kLaneK < kdim, acc);
+}
+
+// ---------------------------------------------------------------------------
+// up: gate/up SwiGLU rows (HIT, shared) or A_e rows (LORE)
+// ---------------------------------------------------------------------------
+template <int DT, int NB, bool kUp>
+__device__ __forceinline__ void up_pass(const char* gate, const char* up, const char* const (&xb)[NB], int kdim, int w,
+                                        int quad, f32x4_t (&red)[kWaves][kTokTiles][2][64], int lane) {
+    if constexpr (kUp) {
+        const char* const a[2] = {gate, up};
+        f32x4_t acc[2][NB];
+        wave_product<DT, 2, NB>(a, xb, kdim, w, quad, acc);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) { red[w][j][0][lane] = acc[0][j]; red[w][j][1][lane] = acc[1][j]; }
+    } else {
+        const char* const a[1] = {gate};
+        f32x4_t acc[1][NB];
+        wave_product<DT, 1, NB>(a, xb, kdim, w, quad, acc);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) red[w][j][0][lane] = acc[0][j];
+    }
+}
+
+template <int DT>
+__device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x4_t (&red)[kWaves][kTokTiles][2][64]) {
+    using T_ = Tr<DT>;
+    constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const void* wbase;
+    size_t gate_row0, up_row0;
+    int nrows, start = 0, n = a.T;
+    if (tile.kind == kKindHit) {
+        start = g.start;
+        n = g.n;
+        wbase = a.w13_pool;
+        nrows = a.I;
+        gate_row0 = (size_t)g.slot * 2 * a.I;
+        up_row0 = gate_row0 + a.I;
+    } else if (tile.kind == kKindShared) {
+        wbase = a.w13s;
+        nrows = a.Is;
+        gate_row0 = 0;
+        up_row0 = a.Is;
+    } else {
+        start = g.start;
+        n = g.n;
+        wbase = a.lore_A;
+        nrows = a.r;
+        gate_row0 = (size_t)g.e * a.r;
+        up_row0 = gate_row0;
+    }
+    const int m = lane & 15;  // A row / B column owned by this lane
+    const int quad = lane >> 4;
+    // rows past the end of the matrix read its last row; their outputs are dropped
+    const int row = min(tile.rt * 16 + m, nrows - 1);
+    const size_t kb = (size_t)quad * T_::kLaneK * es;  // lane's byte offset inside a step
+    const char* gate = static_cast<const char*>(wbase) + (gate_row0 + row) * (size_t)a.d * es + kb;
+    const char* up = static_cast<const char*>(wbase) + (up_row0 + row) * (size_t)a.d * es + kb;
+
+    for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
+        const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
+        // padding columns read the bucket's last token; their outputs are dropped
+        const int gi0 = min(g0 + m, n - 1), gi1 = min(g0 + 16 + m, n - 1);
+        const int t0 = (tile.kind == kKindShared) ? gi0 : token_of(a, start + gi0);
+        const int t1 = (tile.kind == kKindShared) ? gi1 : token_of(a, start + gi1);
+        const char* const xb[kTokTiles] = {static_cast<const char*>(a.x) + (size_t)t0 * a.d * es + kb,
+                                           static_cast<const char*>(a.x) + (size_t)t1 * a.d * es + kb};
+        const char* const x1[1] = {xb[0]};
+        if (tile.kind == kKindLore) {
+            if (ntt == 1) up_pass<DT, 1, false>(gate, up, x1, a.d, w, quad, red, lane);
+            else up_pass<DT, 2, false>(gate, up, xb, a.d, w, quad, red, lane);
+        } else {
+            if (ntt == 1) up_pass<DT, 1, true>(gate, up, x1, a.d, w, quad, red, lane);
+            else up_pass<DT, 2, true>(gate, up, xb, a.d, w, quad, red, lane);
+        }
+        __syncthreads();
+        if (w < ntt) {
+            const int tt = w;
+            f32x4_t sg = red[0][tt][0][lane], su = red[0][tt][1][lane];
+#pragma unroll
+            for (int ww = 1; ww < kWaves; ++ww) {
+                sg += red[ww][tt][0][lane];
+                if (tile.kind != kKindLore) su += red[ww][tt][1][lane];
+            }
+            const int gi = g0 + tt * 16 + m;  // output column = token of lane m
+            const int orow = tile.rt * 16 + quad * 4;
+            if (gi < n && orow < nrows) {
+                if (tile.kind == kKindLore) {
+                    *reinterpret_cast<f32x4_t*>(a.u + (size_t)(start + gi) * a.r + orow) = sg;
+                } else {
+                    f32x4_t h;
+                    h.x = silu(sg.x) * su.x;
+                    h.y = silu(sg.y) * su.y;
+                    h.z = silu(sg.z) * su.z;
+                    h.w = silu(sg.w) * su.w;
+                    if (tile.kind == kKindHit)
+                        T_::store4(a.h, (size_t)(start + gi) * a.ldh + orow, h);
+                    else
+                        T_::store4(a.hs, (size_t)gi * a.ldhs + orow, h);
+                }
+            }
+        }
+        __syncthreads();
+    }
+}
+
+
+// ---------------------------------------------------------------------------
+// down: W2 rows (HIT, shared) with the MFMA path, B_e rows (LORE) on vector ALUs
+// ---------------------------------------------------------------------------
+template <int DT>
+__device__ void lore_down_tile(const FfnArgs& a, int expert, int start, int n, int rt, float* s_u) {
+    const int tid = threadIdx.x;
+    const int row = rt * kLoreRows + tid;
+    const bool row_ok = row < a.d;
+    const size_t brow = ((size_t)expert * a.d + (row_ok ? row : 0)) * (size_t)a.r;
+    for (int g0 = 0; g0 < n; g0 += kLoreTok) {
+        const int nt = min(kLoreTok, n - g0);
+        for (int i = tid; i < nt * a.r; i += kThreads) {
+            const int j = i / a.r, q = i - j * a.r;
+            s_u[j * a.r + q] = a.u[(size_t)(start + g0 + j) * a.r + q];
+        }
+        __syncthreads();
+        float acc[kLoreTok];
+#pragma unroll
+        for (int j = 0; j < kLoreTok; ++j) acc[j] = 0.f;
+        if (row_ok) {
+            for (int q = 0; q < a.r; q += Tr<DT>::kLaneK) {
+                const u32x4_t raw = Tr<DT>::load(a.lore_B, brow + q);
+                float bv[8];
+                if (DT == SPICE_BF16) {
+                    const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        bv[2 * i] = __uint_as_float(wv[i] << 16);
+                        bv[2 * i + 1] = __uint_as_float(wv[i] & 0xFFFF0000u);
+                    }
+                } else {
+                    bv[0] = __uint_as_float(raw.x); bv[1] = __uint_as_float(raw.y);
+                    bv[2] = __uint_as_float(raw.z); bv[3] = __uint_as_float(raw.w);
+                }
+#pragma unroll
+                for (int j = 0; j < kLoreTok; ++j) {
+                    if (j < nt) {
+#pragma unroll
+                        for (int qq = 0; qq < Tr<DT>::kLaneK; ++qq) acc[j] += bv[qq] * s_u[j * a.r + q + qq];
+                    }
+                }
+            }
+#pragma unroll
+            for (int j = 0; j < kLoreTok; ++j)
+                if (j < nt) a.y_slots[(size_t)(start + g0 + j) * a.d + row] = acc[j];
+        }
+        __syncthreads();
+    }
+}
+
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void down_pass(const char* const (&a)[NA], const char* const (&hb)[NB], int kdim,
+                                          int w, int quad, f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64], int lane) {
+    f32x4_t acc[NA][NB];
+    wave_product<DT, NA, NB>(a, hb, kdim, w, quad, acc);
+#pragma unroll
+    for (int rr = 0; rr < NA; ++rr)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) red[w][rr][j][lane] = acc[rr][j];
+}
+
+template <int DT>
+__device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
+                          f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64]) {
+    using T_ = Tr<DT>;
+    constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const void* wbase;
+    const void* hbase;
+    int kdim, start = 0, n = a.T;
+    size_t row0;
+    if (tile.kind == kKindHit) {
+        start = g.start;
+        n = g.n;
+        wbase = a.w2_pool;
+        hbase = a.h;
+        kdim = a.I;
+        row0 = (size_t)g.slot * a.d;
+    } else {
+        wbase = a.w2s;
+        hbase = a.hs;
+        kdim = a.Is;
+        row0 = 0;
+    }
+    const int m = lane & 15, quad = lane >> 4;
+    const int nrt = kDownRows;
+    const int dim0 = tile.rt * 16 * kDownRows;
+    const size_t kb = (size_t)quad * T_::kLaneK * es;
+    const char* const aw[kDownRows] = {
+        // tail rows read the last row; their outputs are dropped
+        static_cast<const char*>(wbase) + (row0 + min(dim0 + m, a.d - 1)) * (size_t)kdim * es + kb,
+        static_cast<const char*>(wbase) + (row0 + min(dim0 + 16 + m, a.d - 1)) * (size_t)kdim * es + kb};
+    for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
+        const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
+        const int hs0 = (tile.kind == kKindShared) ? 0 : start;
+        const size_t ld = (tile.kind == kKindShared) ? a.ldhs : a.ldh;
+        const char* const hb[kTokTiles] = {
+            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + m, n - 1)) * ld * es + kb,
+            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + 16 + m, n - 1)) * ld * es + kb};
+        const char* const a1[1] = {aw[0]};
+        const char* const h1[1] = {hb[0]};
+        if (nrt == 1) {
+            if (ntt == 1) down_pass<DT, 1, 1>(a1, h1, kdim, w, quad, red, lane);
+            else down_pass<DT, 1, 2>(a1, hb, kdim, w, quad, red, lane);
+        } else {
+            if (ntt == 1) down_pass<DT, kDownRows, 1>(aw, h1, kdim, w, quad, red, lane);
+            else down_pass<DT, kDownRows, 2>(aw, hb, kdim, w, quad, red, lane);
+        }
+        __syncthreads();
+        // wave w finalises (row tile, token tile) pair w
+        const int rr = w % kDownRows, tt = w / kDownRows;
+        if (tt < ntt && rr < nrt) {
+            f32x4_t s = red[0][rr][tt][lane];
+#pragma unroll
+            for (int ww = 1; ww < kWaves; ++ww) s += red[ww][rr][tt][lane];
+            const int gi = g0 + tt * 16 + m;
+            const int dim = dim0 + rr * 16 + quad * 4;
+            if (gi < n && dim < a.d) {
+                float* dst = (tile.kind == kKindShared) ? a.y_shared + (size_t)gi * a.d
+                                                        : a.y_slots + (size_t)(start + gi) * a.d;
+                *reinterpret_cast<f32x4_t*>(dst + dim) = s;
+            }
+        }
+        __syncthreads();
+    }
+}
+
+
+}  // namespace
+}  // namespace spice

@@ -202,7 +202,7 @@ extern "C" spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, in
         // exact slots grouped by expert, ascending slot id inside a group
         std::vector<int> count(N, 0);
         for (size_t s = 0; s < S; ++s) {
-            if (slot_class_host[s] > SPICE_CLASS_EXACT)
+            if (slot_class_host[s] > SPICE_CLASS_EXACT_GPU)
                 return spice::set_error(SPICE_ERR_INVALID, "moe_exact_residual_host: slot_class out of range");
             if (slot_class_host[s] != SPICE_CLASS_EXACT) continue;
             const int e = topk_idx_host[s];

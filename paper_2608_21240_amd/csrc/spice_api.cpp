@@ -298,6 +298,47 @@ spice_status_t lore_surrogate_apply(const spice_moe_cfg_t* cfg, int32_t T, const
     SPICE_TRY_END
 }
 
+spice_status_t moe_expert_ffn_fetched(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
+                                      const int32_t* offsets, uint8_t* slot_class, const int32_t* fetch_expert,
+                                      const void* w13_fetch, const void* w2_fetch, int32_t n_slots,
+                                      float* y_slots, void* ws, size_t ws_bytes, spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    spice_status_t st = check_cfg(cfg);
+    if (st != SPICE_OK) return st;
+    const spice_moe_cfg_t& c = *cfg;
+    if ((st = check_tokens(c, T)) != SPICE_OK) return st;
+    if (n_slots < 1 || n_slots > c.n_experts)
+        return fail(SPICE_ERR_INVALID, "moe_expert_ffn_fetched: n_slots must be in [1, n_experts]");
+    if (T == 0) return SPICE_OK;
+    SPICE_REQUIRE(x, "x");
+    SPICE_REQUIRE(perm, "perm");
+    SPICE_REQUIRE(offsets, "offsets");
+    SPICE_REQUIRE(slot_class, "slot_class");
+    SPICE_REQUIRE(fetch_expert, "fetch_expert");
+    SPICE_REQUIRE(w13_fetch, "w13_fetch");
+    SPICE_REQUIRE(w2_fetch, "w2_fetch");
+    SPICE_REQUIRE(y_slots, "y_slots");
+    if ((st = check_ws(c, T, ws, ws_bytes)) != SPICE_OK) return st;
+    if (overlaps(y_slots, (size_t)T * c.top_k * c.d * sizeof(float), x, (size_t)T * c.d * elem_size(c)))
+        return fail(SPICE_ERR_INVALID, "moe_expert_ffn_fetched: y_slots aliases x");
+    const spice::WsLayout L = spice::ws_layout(c, T);
+    char* wsb = static_cast<char*>(ws);
+    spice::FfnArgs a{};
+    a.T = T; a.d = c.d; a.N = c.n_experts; a.K = c.top_k; a.C = n_slots; a.I = c.inter;
+    a.Is = c.shared_inter; a.r = c.lore_rank; a.dtype = c.dtype; a.groups = spice::kDoHit;
+    a.ldh = c.inter + spice::kHPad; a.ldhs = c.shared_inter + spice::kHPad;
+    a.x = x; a.perm = perm; a.offsets = offsets; a.resident_slot = nullptr;
+    a.w13_pool = w13_fetch; a.w2_pool = w2_fetch; a.y_slots = y_slots;
+    a.h = wsb + L.h; a.hs = wsb + L.hs; a.u = reinterpret_cast<float*>(wsb + L.u);
+    a.ctrl = reinterpret_cast<uint32_t*>(wsb);
+    spice::FetchArgs f{};
+    f.fetch_expert = fetch_expert; f.slot_class = slot_class; f.n_slots = n_slots;
+    hipError_t e = spice::launch_expert_ffn_fetched(a, f, stream);
+    if (e != hipSuccess) return hip_fail(e, "moe_expert_ffn_fetched");
+    return SPICE_OK;
+    SPICE_TRY_END
+}
+
 spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w, const uint8_t* slot_class,
                            const int32_t* inv_perm, const float* y_slots, const float* y_shared, const float* resid,
                            void* out, spice_stream_t stream) {

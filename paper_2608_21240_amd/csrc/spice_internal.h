@@ -90,6 +90,15 @@ struct FfnArgs {
     uint32_t* ctrl;
 };
 
+// The fetched-expert FFN (M_fetch of Eq. 12): fetch slot j serves the bucket
+// (EXACT, fetch_expert[j]) with the weights in slot j of the fetch pool (passed as
+// the FfnArgs pools), and relabels that bucket's slots EXACT -> EXACT_GPU.
+struct FetchArgs {
+    const int32_t* fetch_expert;  // device [n_slots], -1 = unused slot
+    uint8_t* slot_class;          // device [T*K]
+    int32_t n_slots;
+};
+
 struct CombineArgs {
     int32_t T, d, K, dtype;
     const float* topk_w;
@@ -129,6 +138,7 @@ hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+hipError_t launch_expert_ffn_fetched(const FfnArgs& a, const FetchArgs& f, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, size_t words, uint32_t value, hipStream_t s);
 

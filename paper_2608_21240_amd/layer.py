@@ -128,13 +128,16 @@ class DeviceLayer:
                 A, B = host.lore(e)
                 self.lore_A[e].copy_(to_tensor(A, dt))
                 self.lore_B[e].copy_(to_tensor(B, dt))
-        # host-resident weights of the non-resident experts (the exact CPU path)
+        # host-resident weights of the non-resident experts (the exact CPU path), pinned so
+        # that fetching them to the GPU (the exact-miss split) copies asynchronously
         self.host_w13: List = [None] * s.n_experts
         self.host_w2: List = [None] * s.n_experts
         if host_exact:
             for e in range(s.n_experts):
                 if slot[e] < 0:
-                    self.host_w13[e], self.host_w2[e] = host.expert(e)
+                    w13, w2 = host.expert(e)
+                    self.host_w13[e] = to_tensor(w13, dt, pin=True)
+                    self.host_w2[e] = to_tensor(w2, dt, pin=True)
 
     def hbm_bytes(self) -> int:
         ts = [self.wg, self.w13s, self.w2s, self.w13_pool, self.w2_pool, self.lore_A, self.lore_B]
@@ -145,7 +148,7 @@ class LayerRun:
     """Buffers and streams for layer calls with up to T tokens."""
 
     def __init__(self, shape, T: int, n_slots: int, tau: float = 0.5, conf_mode: int = 0, norm_topk: int = 0,
-                 device: str = "cuda", keep_logits: bool = False):
+                 device: str = "cuda", keep_logits: bool = False, fetch_slots: int = 0):
         self.shape, self.T = shape, T
         self.cfg = spice.make_cfg(shape, n_slots, tau, conf_mode, norm_topk)
         s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
@@ -175,6 +178,19 @@ class LayerRun:
         self.resid = torch.zeros((T, d), dtype=torch.float32).pin_memory()
         self.host_out = spice.host_out(self.x_host, self.idx_host, self.w_host, self.cls_host, self.counts_host)
         self.e_route = torch.cuda.Event()
+        # fetch pool of the exact-miss split (Eq. 12: M_fetch), if any
+        self.fetch_slots = fetch_slots
+        if fetch_slots:
+            td = torch_dtype(s.dtype)
+            self.w13_fetch = torch.empty((fetch_slots, 2 * s.inter, d), dtype=td, device=device)
+            self.w2_fetch = torch.empty((fetch_slots, d, s.inter), dtype=td, device=device)
+            self.fetch_expert = torch.full((fetch_slots,), -1, dtype=torch.int32, device=device)
+            self.fetch_stage = torch.full((fetch_slots,), -1, dtype=torch.int32).pin_memory()
+            self.copy_stream = torch.cuda.Stream(device=device)
+            self.e_fetched = torch.cuda.Event()
+            self.e_pool_free = torch.cuda.Event()
+            self.e_pool_free.record(torch.cuda.current_stream())
+        self.last_fetch: List[int] = []
 
     # -- the steps, each one C-ABI call ------------------------------------------------
     def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
@@ -204,17 +220,39 @@ class LayerRun:
         spice.moe_combine(self.cfg, T, self.topk_w, self.slot_class, self.inv_perm, self.y_slots, self.y_shared,
                           resid, self.out)
 
-    def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0):
-        """Wait for the route kernel's host copies, then the CPU residual into self.resid."""
+    def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0, split=None):
+        """Wait for the route kernel's host copies; with a split cost model, fetch the experts
+        the planner picks and queue their FFN on the GPU; then the CPU residual of the other
+        exact misses into self.resid."""
         self.e_route.synchronize()
+        self.last_fetch = []
+        if split is not None and self.fetch_slots:
+            cls = self.cls_host[:T].numpy()
+            fetch = spice.moe_split_plan(self.cfg, T, self.idx_host[:T].numpy(), cls, split, self.fetch_slots)
+            if fetch:
+                self.last_fetch = fetch
+                with torch.cuda.stream(self.copy_stream):
+                    self.copy_stream.wait_event(self.e_pool_free)  # the previous fetched FFN is done with the pool
+                    spice.moe_fetch_experts(self.cfg, fetch, L.host_w13, L.host_w2, self.w13_fetch, self.w2_fetch,
+                                            self.fetch_slots, self.fetch_expert, self.fetch_stage)
+                    self.e_fetched.record(self.copy_stream)
+                cur = torch.cuda.current_stream()
+                cur.wait_event(self.e_fetched)
+                spice.moe_expert_ffn_fetched(self.cfg, T, self.x_cur, self.perm, self.offsets, self.slot_class,
+                                             self.fetch_expert, self.w13_fetch, self.w2_fetch, self.fetch_slots,
+                                             self.y_slots, self.ws, self.ws_bytes)
+                self.e_pool_free.record(cur)
         spice.moe_exact_residual_host(self.cfg, T, self.x_host, self.idx_host, self.w_host, self.cls_host,
                                       L.host_w13, L.host_w2, self.resid, n_threads)
 
     def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
-                exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None):
-        """One layer call: route, FFN + LoRE on the GPU overlapped with the exact CPU residual, combine."""
+                exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None,
+                split=None):
+        """One layer call: route, FFN + LoRE on the GPU overlapped with the exact CPU residual
+        (and, with a split cost model, the fetched exact misses on the GPU), combine."""
         T = self.T if T is None else T
         ev = events or {}
+        self.x_cur = x
         if "start" in ev:
             ev["start"].record()
         self.route(L, x, conf, T, to_host=exact)
@@ -226,7 +264,7 @@ class LayerRun:
         if "experts" in ev:
             ev["experts"].record()
         if exact:
-            self.exact_host(L, T, n_threads)
+            self.exact_host(L, T, n_threads, split)
         if "resid" in ev:
             ev["resid"].record()
         self.combine(self.resid if exact else None, T)

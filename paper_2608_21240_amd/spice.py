@@ -19,7 +19,7 @@ SPICE_OK, SPICE_ERR_INVALID, SPICE_ERR_UNSUPPORTED, SPICE_ERR_HIP, SPICE_ERR_WOR
     0, -1, -2, -3, -4, -5)
 SPICE_F32, SPICE_BF16 = 0, 1
 SPICE_CONF_INPUT, SPICE_CONF_GATE, SPICE_CONF_GATE_RENORM = 0, 1, 2
-SPICE_CLASS_HIT, SPICE_CLASS_LORE, SPICE_CLASS_EXACT = 0, 1, 2
+SPICE_CLASS_HIT, SPICE_CLASS_LORE, SPICE_CLASS_EXACT, SPICE_CLASS_EXACT_GPU = 0, 1, 2, 3
 SPICE_MAX_EXPERTS, SPICE_MAX_TOKENS, SPICE_MAX_LORE_RANK = 256, 65536, 256
 SPICE_WS_CONTROL_BYTES = 131072
 SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
@@ -29,7 +29,8 @@ EXPORTS = (
     "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
     "moe_route_bucket", "moe_expert_ffn_grouped", "lore_surrogate_apply", "moe_combine",
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
-    "moe_cache_destroy", "spice_status_string", "spice_last_error",
+    "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
+    "spice_status_string", "spice_last_error",
 )
 
 
@@ -44,6 +45,12 @@ class spice_moe_cfg_t(ctypes.Structure):
                 ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
                 ("n_slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32),
                 ("conf_mode", ctypes.c_int32), ("tau", ctypes.c_float)]
+
+
+class spice_split_cost_t(ctypes.Structure):
+    _fields_ = [("cpu_bytes_per_s", ctypes.c_double), ("cpu_flops_per_s", ctypes.c_double),
+                ("pcie_bytes_per_s", ctypes.c_double), ("gpu_fixed_s", ctypes.c_double),
+                ("margin", ctypes.c_double)]
 
 
 class spice_host_out_t(ctypes.Structure):
@@ -88,6 +95,10 @@ def lib() -> ctypes.CDLL:
             "moe_cache_wait": (_I, [_P, _I, _P]),
             "moe_cache_state": (_I, [_P, _I, _P, _P]),
             "moe_cache_destroy": (None, [_P]),
+            "moe_split_plan": (_I, [C, _I, _P, _P, ctypes.POINTER(spice_split_cost_t), _I, _P,
+                                    ctypes.POINTER(_I)]),
+            "moe_fetch_experts": (_I, [C, _I, _P, _P, _P, _P, _P, _I, _P, _P, _P]),
+            "moe_expert_ffn_fetched": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I, _P, _P, _Z, _P]),
             "spice_status_string": (ctypes.c_char_p, [_I]),
             "spice_last_error": (ctypes.c_char_p, []),
         }
@@ -259,3 +270,32 @@ class ExpertCache:
             self.close()
         except Exception:
             pass
+
+
+def moe_split_plan(cfg, T, topk_idx_host, slot_class_host, cost: spice_split_cost_t, max_fetch: int):
+    """-> list of experts to fetch; slot_class_host (uint8 array) is relabelled in place."""
+    import numpy as np
+
+    out = np.empty(max(max_fetch, 1), np.int32)
+    n = ctypes.c_int32(0)
+    _check("moe_split_plan", lib().moe_split_plan(
+        ctypes.byref(cfg), T, _p(topk_idx_host), _p(slot_class_host), ctypes.byref(cost), max_fetch, _p(out),
+        ctypes.byref(n)))
+    return out[:n.value].tolist()
+
+
+def moe_fetch_experts(cfg, experts: Sequence[int], w13_host: Sequence, w2_host: Sequence, w13_fetch, w2_fetch,
+                      n_slots: int, fetch_expert, fetch_expert_stage, copy_stream=None) -> None:
+    ex = (ctypes.c_int32 * max(len(experts), 1))(*experts)
+    t13 = (ctypes.c_void_p * len(w13_host))(*[_p(w) for w in w13_host])
+    t2 = (ctypes.c_void_p * len(w2_host))(*[_p(w) for w in w2_host])
+    _check("moe_fetch_experts", lib().moe_fetch_experts(
+        ctypes.byref(cfg), len(experts), ex, t13, t2, _p(w13_fetch), _p(w2_fetch), n_slots, _p(fetch_expert),
+        _p(fetch_expert_stage), _stream(copy_stream)))
+
+
+def moe_expert_ffn_fetched(cfg, T, x, perm, offsets, slot_class, fetch_expert, w13_fetch, w2_fetch, n_slots,
+                           y_slots, ws, ws_bytes, stream=None) -> None:
+    _check("moe_expert_ffn_fetched", lib().moe_expert_ffn_fetched(
+        ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(slot_class), _p(fetch_expert), _p(w13_fetch),
+        _p(w2_fetch), n_slots, _p(y_slots), _p(ws), ws_bytes, _stream(stream)))

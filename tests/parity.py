@@ -64,18 +64,18 @@ class Case:
 
     # ---------------------------------------------------------------- HIP path
     def run_gpu(self, dev: Optional[LY.DeviceLayer] = None, fused: bool = True, exact: bool = True,
-                run: Optional[LY.LayerRun] = None, n_threads: int = 0):
+                run: Optional[LY.LayerRun] = None, n_threads: int = 0, split=None, fetch_slots: int = 0):
         s = self.shape
         self.dev = dev if dev is not None else LY.DeviceLayer(self.host, n_slots=self.n_slots)
         self.run = run if run is not None else LY.LayerRun(s, self.T, self.dev.C, tau=self.wl.tau,
                                                             conf_mode=self.wl.conf_mode, norm_topk=self.wl.norm_topk,
-                                                            keep_logits=True)
+                                                            keep_logits=True, fetch_slots=fetch_slots)
         R = self.run
         xd = LY.to_tensor(self.x, s.dtype, "cuda")
         conf = torch.from_numpy(np.ascontiguousarray(self.conf)).cuda()
         R.y_slots.zero_(); R.y_shared.zero_()
         if fused:
-            R.forward(self.dev, xd, conf, self.T, exact=exact, n_threads=n_threads)
+            R.forward(self.dev, xd, conf, self.T, exact=exact, n_threads=n_threads, split=split)
         else:
             R.route(self.dev, xd, conf, self.T, to_host=exact)
             R.experts(self.dev, xd, self.T, fuse_lore=False)

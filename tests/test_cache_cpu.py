@@ -113,7 +113,7 @@ def test_errors_leave_state_unchanged():
         spice.ExpertCache(cfg, 1, [[0, 1, 2]], load=True)  # load needs pools
     c = spice.ExpertCache(cfg, 2, [[0, 1, 2], [3, 4, -1]])
     before = [c.state(l) for l in range(2)]
-    for bad_idx, bad_cls in (([[0, 9]], [[HIT, EXACT]]), ([[0, 5]], [[HIT, 3]])):
+    for bad_idx, bad_cls in (([[0, 9]], [[HIT, EXACT]]), ([[0, 5]], [[HIT, 4]])):
         with pytest.raises(spice.SpiceError):
             c.step(0, 0, np.array(bad_idx), np.array(bad_cls), 2)
     with pytest.raises(spice.SpiceError):

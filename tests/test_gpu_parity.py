@@ -226,3 +226,40 @@ def test_host_copies_match_device_outputs(shape, T, R):
     assert run.counts_host.tolist() == np.bincount(c.g["cls"].reshape(-1), minlength=3).tolist()
     from parity import to_np
     assert np.array_equal(to_np(run.x_host[:T]), c.x)
+
+
+FORCE_FETCH = dict(cpu_bytes_per_s=1e8, cpu_flops_per_s=1e12, pcie_bytes_per_s=1e13, gpu_fixed_s=0.0, margin=0.0)
+
+
+@pytest.mark.parametrize("shape,T,R,slots", [(W.small_shape(), 24, 5, 3), (RAGGED_BF16, 37, 6, 4),
+                                             (RAGGED_F32, 41, 4, 2)])
+def test_exact_split_fetched_experts_on_gpu(shape, T, R, slots):
+    """Eq. 12's M_fetch: the planner moves some exact misses to the GPU (a cost model that
+    makes fetching pay); outputs still match the oracle, whose result does not depend on
+    where an exact miss runs."""
+    from paper_2608_21240_amd import spice
+    say(f"exact split d={shape.d} T={T} R={R} fetch slots={slots}")
+    c = Case(small_wl(shape, T, R))
+    cost = spice.spice_split_cost_t(**FORCE_FETCH)
+    c.run_gpu(split=cost, fetch_slots=slots)
+    c.run_oracle()
+    fetched = c.run.last_fetch
+    assert 0 < len(fetched) <= slots
+    o, g = c.o, c.g
+    exact_e = set(o["idx"][o["cls"] == EXACT].tolist())
+    assert set(fetched) <= exact_e
+    on_gpu = np.isin(o["idx"], fetched) & (o["cls"] == EXACT)
+    # fetched slots are relabelled on the device and on the host, the rest is the oracle's routing
+    assert (g["cls"][on_gpu] == spice.SPICE_CLASS_EXACT_GPU).all()
+    assert np.array_equal(g["cls"][~on_gpu], o["cls"][~on_gpu])
+    assert np.array_equal(c.run.cls_host[:T].numpy(), g["cls"])
+    assert np.array_equal(g["idx"], o["idx"]) and np.array_equal(g["perm"], o["perm"])
+    # the layer output covers every exact miss, wherever it ran; fetched slots' expert
+    # outputs are the oracle's expert outputs
+    from parity import as_f64, rel_err, tol_for
+    errs_out = rel_err(as_f64(g["out"], shape.dtype)[o["tokens"]], o["out"])
+    assert errs_out.max() <= tol_for(shape), errs_out.max()
+    ys = np.array([g["y_slots"][g["inv_perm"][t * shape.top_k + k]] for t, k in np.argwhere(on_gpu)])
+    refs = np.array([o["y_slot"][t, k] for t, k in np.argwhere(on_gpu)])
+    assert rel_err(ys, refs).max() <= tol_for(shape)
+    assert c.run.flags() == 0

@@ -85,9 +85,28 @@ def test_degenerate_inputs(orc):
         spice.moe_exact_residual_host(c, 6, x, rt["idx"], rt["g"].astype(np.float32), rt["cls"], [None] * 16,
                                       [None] * 16, out)
     assert e.value.status == spice.SPICE_ERR_INVALID
-    bad = rt["cls"].copy(); bad[0, 0] = 3
+    bad = rt["cls"].copy(); bad[0, 0] = 4
     with pytest.raises(spice.SpiceError):
         spice.moe_exact_residual_host(c, 6, x, rt["idx"], rt["g"].astype(np.float32), bad, w13, w2, out)
     badi = rt["idx"].copy(); badi[rt["cls"] == EXACT] = 99
     with pytest.raises(spice.SpiceError):
         spice.moe_exact_residual_host(c, 6, x, badi, rt["g"].astype(np.float32), rt["cls"], w13, w2, out)
+
+
+def test_exact_gpu_slots_are_left_to_the_gpu(orc):
+    """Slots relabelled EXACT_GPU (fetched experts, Eq. 12's M_fetch) are skipped: the
+    residual equals the oracle's over the remaining EXACT slots only."""
+    shape = W.small_shape()
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, 9, 5)
+    c = spice.make_cfg(shape, n_slots=0)
+    cls = rt["cls"].copy()
+    ex = np.argwhere(cls == EXACT)
+    assert len(ex) >= 2
+    for t, k in ex[::2]:
+        cls[t, k] = spice.SPICE_CLASS_EXACT_GPU
+    out = np.empty((9, shape.d), np.float32)
+    spice.moe_exact_residual_host(c, 9, x, rt["idx"], rt["g"].astype(np.float32), cls, w13, w2, out)
+    only = np.where(cls == EXACT, EXACT, LORE).astype(np.uint8)
+    ref = orc.exact_residual(orc.make_cfg(shape), x, rt["idx"], rt["g"], only, w13, w2)
+    err = np.abs(out - ref).max() / max(np.abs(ref).max(), 1e-30)
+    assert err < 1e-4 if shape.dtype == 0 else err < 2e-2
