@@ -243,45 +243,59 @@ def main():
 
 def calibrate_split(run, dev, shape, T, args):
     """Cost model of the exact-miss split measured on this host, from the routing copies
-    of the last call on `dev`.
+    of the last call on `dev` (restored afterwards).
 
-    CPU: two timed residual calls over the same exact-miss experts, one with every exact
-    slot and one with only each expert's first slot (the other slots masked out), give the
-    rate over expert weights and the arithmetic rate per token (best of two each).
-    PCIe: one untimed fetch, then the best of two timed fetches into the pool."""
+    CPU arithmetic rate: one exact expert serving every token against the same expert
+    serving one token.  CPU rate over expert weights: every exact expert of the call with
+    one token each, less that arithmetic.  PCIe: one untimed fetch, then the best of two
+    timed fetches into the pool.  Host timings are the best of three calls."""
     import torch
 
     from paper_2608_21240_amd import spice
 
-    idx = run.idx_host[:T].numpy()
-    cls_all = run.cls_host[:T].numpy().copy()
-    exact = sorted(set(idx[cls_all == 2].tolist()))
+    idx0 = run.idx_host[:T].numpy().copy()
+    cls0 = run.cls_host[:T].numpy().copy()
+    exact = sorted(set(idx0[cls0 == 2].tolist()))
     if not exact:
         return None
-    first = np.full(cls_all.shape, 1, np.uint8)  # LoRE slots are not the host's work
-    seen = set()
-    for t, k in zip(*np.nonzero(cls_all == 2)):
-        if idx[t, k] not in seen:
-            seen.add(idx[t, k])
-            first[t, k] = 2
+    lore = np.full(cls0.shape, 1, np.uint8)  # LoRE slots are not the host's work
 
-    def cpu_time(cls):
+    def cpu_time(idx, cls):
+        run.idx_host[:T].copy_(torch.from_numpy(idx))
         run.cls_host[:T].copy_(torch.from_numpy(cls))
         best = float("inf")
-        for _ in range(2):
+        for _ in range(3):
             t0 = time.perf_counter()
             spice.moe_exact_residual_host(run.cfg, T, run.x_host, run.idx_host, run.w_host, run.cls_host,
                                           dev.host_w13, dev.host_w2, run.resid, args.threads)
             best = min(best, time.perf_counter() - t0)
         return best
 
-    t_all, t_first = cpu_time(cls_all), cpu_time(first)
-    run.cls_host[:T].copy_(torch.from_numpy(cls_all))
-    n_slots, n_exp = int((cls_all == 2).sum()), len(exact)
     flops_tok = 6.0 * shape.inter * shape.d
-    extra = t_all - t_first
-    cpu_flops = (n_slots - n_exp) * flops_tok / extra if n_slots > n_exp and extra > 0 else 1e18
-    cpu_bytes = n_exp * shape.expert_bytes / max(t_first - n_exp * flops_tok / cpu_flops, 1e-9)
+    cpu_flops = 1e18  # one token: the arithmetic cannot be told apart; the byte rate absorbs it
+    e0 = exact[0]
+    if T >= 4:
+        # slot k = 0 of every token goes to e0: no token lists an expert twice, since the
+        # other slots of a token are masked to LoRE
+        many_i, many_c = idx0.copy(), lore.copy()
+        many_i[:, 0] = e0
+        many_c[:, 0] = 2
+        one_c = lore.copy()
+        one_c[0, 0] = 2
+        extra = cpu_time(many_i, many_c) - cpu_time(many_i, one_c)
+        if extra > 0:
+            cpu_flops = (T - 1) * flops_tok / extra
+    first = lore.copy()
+    seen = set()
+    for t, k in zip(*np.nonzero(cls0 == 2)):
+        if idx0[t, k] not in seen:
+            seen.add(idx0[t, k])
+            first[t, k] = 2
+    t_first = cpu_time(idx0, first)
+    n_exp = len(exact)
+    cpu_bytes = n_exp * shape.expert_bytes / max(t_first - n_exp * flops_tok / cpu_flops, 0.2 * t_first)
+    run.idx_host[:T].copy_(torch.from_numpy(idx0))
+    run.cls_host[:T].copy_(torch.from_numpy(cls0))
     probe = [e for e in range(shape.n_experts) if dev.host_w13[e] is not None][: min(4, run.fetch_slots)]
 
     def fetch_time():
