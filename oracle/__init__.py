@@ -80,6 +80,17 @@ def _declare(L: ctypes.CDLL) -> None:
     L.orc_exact_residual.restype = _I
     L.orc_lru_step.argtypes = [_I, _I, _P, _P, _I, _I, _I, _P, _P, _I, _P, _P]
     L.orc_lru_step.restype = _I
+    L.orc_round_to.argtypes = [_I, ctypes.c_double]
+    L.orc_round_to.restype = ctypes.c_double
+    L.orc_spec_step.argtypes = [cp, _I, _I, _I, ctypes.c_double, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                _P, _P]
+    L.orc_spec_step.restype = _I
+    L.orc_h_min.argtypes = [ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double, _I,
+                            ctypes.c_double]
+    L.orc_h_min.restype = _I
+    L.orc_prefetch_queue.argtypes = [_I, _I, _I, _I, _P, _P, _I, _P, _P]
+    L.orc_lru_prefetch.argtypes = [_I, _I, _P, _P, _I, _I, _P, _I, _P, _P]
+    L.orc_lru_prefetch.restype = _I
 
 
 def _ptr(a: Optional[np.ndarray]):
@@ -203,6 +214,14 @@ class LRUState:
                                _ptr(idx), _ptr(cls), max_admit, _ptr(adm), _ptr(ev))
         return adm[:n].copy(), ev[:n].copy()
 
+    def prefetch(self, step: int, experts, max_prefetch: int):
+        """Speculative admissions (the prefetch queue of one future layer)."""
+        ex = _c(experts, np.int32).reshape(-1)
+        adm = np.empty(max(max_prefetch, 1), np.int32); ev = np.empty(max(max_prefetch, 1), np.int32)
+        n = lib().orc_lru_prefetch(self.N, self.C, _ptr(self.slot_expert), _ptr(self.last_use), step, len(ex),
+                                   _ptr(ex), max_prefetch, _ptr(adm), _ptr(ev))
+        return adm[:n].copy(), ev[:n].copy()
+
     def resident_mask(self) -> np.ndarray:
         m = np.zeros(self.N, np.int32)
         m[self.slot_expert[self.slot_expert >= 0]] = 1
@@ -233,3 +252,62 @@ def layer(cfg: Cfg, x, wg, bias, resident_mask, conf_in, w13, w2, w13s, w2s, lA,
                                                w13, w2, w13s, w2s, lA, lB)
     r.update(out=out, y_shared=ys, y_slot=yslot, tokens=np.array(toks, np.int32))
     return r
+
+
+# ---- speculative prefetching (Sec. 4.1, Eq. 2-5, Alg. 1) -----------------------------------
+
+def round_to(dtype: int, v: float) -> float:
+    return lib().orc_round_to(dtype, float(v))
+
+
+def spec_step(cfg: Cfg, h_in, delta: int, l_min: int, tau: float, last: bool, wg, bias, w13s, w2s, lA, lB,
+              halted):
+    """One depth of the draft rollout (Alg. 1) for every token.  h_in: storage array [T][d];
+    halted: int32 [T], updated in place.  Returns (pred_idx, pred_prob, conf, h_out)."""
+    h_in = _store(h_in, cfg.dtype)
+    T = h_in.shape[0]
+    wg = _store(wg, cfg.dtype)
+    b = None if bias is None else _c(bias, np.float32)
+    tA, k1 = _table(lA, cfg.dtype); tB, k2 = _table(lB, cfg.dtype)
+    s13, s2 = _store(w13s, cfg.dtype), _store(w2s, cfg.dtype)
+    assert halted.dtype == np.int32 and halted.flags.c_contiguous
+    pidx = np.empty((T, cfg.top_k), np.int32); pprob = np.empty((T, cfg.top_k)); conf = np.empty(T)
+    h_out = np.empty_like(h_in)
+    rc = lib().orc_spec_step(ctypes.byref(cfg), T, delta, l_min, tau, int(last), _ptr(h_in), _ptr(wg), _ptr(b),
+                             _ptr(s13), _ptr(s2), tA, tB, _ptr(halted), _ptr(pidx), _ptr(pprob), _ptr(conf),
+                             _ptr(h_out))
+    if rc != 0:
+        raise ValueError("oracle: a needed LoRE factor was not supplied")
+    return pidx, pprob, conf, h_out
+
+
+def spec_rollout(cfg: Cfg, x, layers, l_min: int, tau: float):
+    """Alg. 1 from anchor x over len(layers) future layers; layers[j] = dict(wg, bias, w13s,
+    w2s, lA, lB) of layer l + 1 + j.  Returns per-depth predictions, confidences, the draft
+    states after each depth, and each token's last enqueued depth."""
+    T = x.shape[0]
+    halted = np.zeros(T, np.int32)
+    h = _store(x, cfg.dtype)
+    out = dict(idx=[], prob=[], conf=[], h=[])
+    depth = np.zeros(T, np.int32)
+    for j, L in enumerate(layers):
+        delta = j + 1
+        was = halted.copy()
+        pidx, pprob, conf, h = spec_step(cfg, h, delta, l_min, tau, delta == len(layers), L["wg"], L.get("bias"),
+                                         L["w13s"], L["w2s"], L["lA"], L["lB"], halted)
+        depth[was == 0] = delta
+        out["idx"].append(pidx); out["prob"].append(pprob); out["conf"].append(conf); out["h"].append(h)
+    return {k: np.stack(v) for k, v in out.items()} | dict(depth=depth)
+
+
+def h_min(P: float, M_e: float, B: float, t_attn: float, K: int, t_expert: float) -> int:
+    return lib().orc_h_min(P, M_e, B, t_attn, K, t_expert)
+
+
+def prefetch_queue(n_experts: int, pred_idx, pred_prob, max_per_depth: int):
+    """Per-depth issue lists of the prefetch intents (Eq. 3)."""
+    pidx = _c(pred_idx, np.int32); pprob = _c(pred_prob, np.float64)
+    D, T, K = pidx.shape
+    ex = np.empty((D, max(max_per_depth, 1)), np.int32); cnt = np.empty(D, np.int32)
+    lib().orc_prefetch_queue(n_experts, D, T, K, _ptr(pidx), _ptr(pprob), max_per_depth, _ptr(ex), _ptr(cnt))
+    return [ex[i, :cnt[i]].tolist() for i in range(D)]

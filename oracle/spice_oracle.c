@@ -11,6 +11,11 @@
  *                                          -> orc_token_output
  *   exact CPU path for M_cpu, Sec. 4.3     -> orc_exact_residual
  *   expert cache bookkeeping (LRU policy)  -> orc_lru_step
+ *   speculative prefetching, Sec. 4.1 and Alg. 1:
+ *     draft rollout depth (Eq. 2, 5; Alg. 1 steps 1-4) -> orc_spec_step
+ *     minimum lookahead, Eq. 4             -> orc_h_min
+ *     prefetch intents, Eq. 3              -> orc_prefetch_queue
+ *     speculative cache admissions         -> orc_lru_prefetch
  */
 #include "spice_oracle.h"
 
@@ -303,5 +308,156 @@ int32_t orc_lru_step(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t
     }
     free(exact_count);
     free(slot_of);
+    return n_adm;
+}
+
+/* ---- Speculative prefetching ------------------------------------------------------- */
+
+double orc_round_to(int32_t dtype, double v) {
+    if (dtype != ORC_BF16) return (double)(float)v;
+    if (v == 0.0 || isnan(v) || isinf(v)) return v;
+    /* bf16 keeps 8 significant bits: round v to a multiple of 2^(e-8), v = m 2^e, m in [0.5, 1) */
+    int e;
+    frexp(v, &e);
+    if (e < -125) e = -125; /* subnormal range of the 8-bit exponent */
+    const double ulp = ldexp(1.0, e - 8);
+    return rint(v / ulp) * ulp; /* rint: to nearest, ties to even (default rounding mode) */
+}
+
+static void store_elem(void* p, int32_t dtype, size_t i, double v) {
+    if (dtype == ORC_BF16) {
+        float f = (float)orc_round_to(ORC_BF16, v); /* exact: a bf16 value is an fp32 value */
+        uint32_t bits;
+        memcpy(&bits, &f, sizeof bits);
+        ((uint16_t*)p)[i] = (uint16_t)(bits >> 16);
+    } else {
+        ((float*)p)[i] = (float)v;
+    }
+}
+
+int32_t orc_spec_step(const orc_cfg_t* c, int32_t T, int32_t delta, int32_t l_min, double tau, int32_t last,
+                      const void* h_in, const void* wg, const float* bias, const void* w13s, const void* w2s,
+                      const void* const* lA, const void* const* lB, int32_t* halted, int32_t* pred_idx,
+                      double* pred_prob, double* conf, void* h_out) {
+    const int32_t d = c->d, N = c->n_experts, K = c->top_k;
+    orc_cfg_t raw = *c;
+    raw.norm_topk = 0; /* pi is the router's own distribution */
+    double* z = (double*)malloc(sizeof(double) * (size_t)N);
+    int32_t* idx = (int32_t*)malloc(sizeof(int32_t) * (size_t)K);
+    double* g = (double*)malloc(sizeof(double) * (size_t)K);
+    double* h = (double*)malloc(sizeof(double) * (size_t)d);
+    double* sh = (double*)malloc(sizeof(double) * (size_t)d);
+    double* dl = (double*)malloc(sizeof(double) * (size_t)d);
+    double* nh = (double*)malloc(sizeof(double) * (size_t)d);
+    int32_t rc = 0;
+    for (int32_t t = 0; t < T && rc == 0; ++t) {
+        const size_t row = (size_t)t * d;
+        for (int32_t i = 0; i < d; ++i) h[i] = elem(h_in, c->dtype, row + i);
+        int32_t update = 0;
+        if (halted[t]) {
+            for (int32_t k = 0; k < K; ++k) {
+                pred_idx[(size_t)t * K + k] = -1;
+                pred_prob[(size_t)t * K + k] = 0.0;
+            }
+            conf[t] = NAN;
+        } else {
+            /* Step 1: the future layer's router on the draft state (Eq. 1, Eq. 2) */
+            orc_router_logits(&raw, 1, (const char*)h_in + row * (c->dtype == ORC_BF16 ? 2 : 4), wg, bias, z, NULL);
+            orc_gates_topk(&raw, 1, z, idx, g, NULL);
+            /* Step 2: enqueue; Step 3: confidence (Eq. 5) and the halting test */
+            double cf = 0.0;
+            for (int32_t k = 0; k < K; ++k) {
+                pred_idx[(size_t)t * K + k] = idx[k];
+                pred_prob[(size_t)t * K + k] = g[k];
+                cf += g[k];
+            }
+            conf[t] = cf;
+            if (delta >= l_min && cf < tau) halted[t] = 1;
+            else update = !last;
+        }
+        if (update) {
+            /* Step 4: h <- Attn(h) + sum_k pi_k (S(h) + B_k A_k h), Attn = identity */
+            orc_swiglu(d, c->shared_inter, c->dtype, w13s, w2s, h, sh);
+            for (int32_t i = 0; i < d; ++i) nh[i] = h[i];
+            for (int32_t k = 0; k < K; ++k) {
+                for (int32_t i = 0; i < d; ++i) dl[i] = 0.0;
+                if (c->lore_rank > 0) {
+                    if (!lA[idx[k]] || !lB[idx[k]]) { rc = -1; break; }
+                    orc_lore_delta(d, c->lore_rank, c->dtype, lA[idx[k]], lB[idx[k]], h, dl);
+                }
+                for (int32_t i = 0; i < d; ++i) nh[i] += g[k] * (sh[i] + dl[i]);
+            }
+            for (int32_t i = 0; i < d; ++i) store_elem(h_out, c->dtype, row + i, nh[i]);
+        } else {
+            for (int32_t i = 0; i < d; ++i) store_elem(h_out, c->dtype, row + i, h[i]);
+        }
+    }
+    free(z); free(idx); free(g); free(h); free(sh); free(dl); free(nh);
+    return rc;
+}
+
+int32_t orc_h_min(double P, double M_e, double B, double t_attn, int32_t K, double t_expert) {
+    const double window = t_attn + (double)K * t_expert;
+    if (!(window > 0.0) || !(B > 0.0)) return -1;
+    return (int32_t)ceil(P * M_e / (B * window));
+}
+
+void orc_prefetch_queue(int32_t n_experts, int32_t n_depth, int32_t T, int32_t K, const int32_t* pred_idx,
+                        const double* pred_prob, int32_t max_per_depth, int32_t* experts, int32_t* counts) {
+    double* mass = (double*)malloc(sizeof(double) * (size_t)n_experts);
+    int32_t* seen = (int32_t*)malloc(sizeof(int32_t) * (size_t)n_experts);
+    for (int32_t dp = 0; dp < n_depth; ++dp) {
+        for (int32_t e = 0; e < n_experts; ++e) { mass[e] = 0.0; seen[e] = 0; }
+        /* Eq. 3: union of the enqueued sets of this depth, with their predicted mass */
+        for (int32_t t = 0; t < T; ++t)
+            for (int32_t k = 0; k < K; ++k) {
+                const size_t i = ((size_t)dp * T + t) * K + k;
+                if (pred_idx[i] < 0) continue;
+                seen[pred_idx[i]] = 1;
+                mass[pred_idx[i]] += pred_prob[i];
+            }
+        int32_t n = 0;
+        while (n < max_per_depth) {
+            int32_t best = -1;
+            for (int32_t e = 0; e < n_experts; ++e)
+                if (seen[e] && (best < 0 || mass[e] > mass[best])) best = e;
+            if (best < 0) break;
+            seen[best] = 0;
+            experts[(size_t)dp * max_per_depth + n++] = best;
+        }
+        counts[dp] = n;
+    }
+    free(mass);
+    free(seen);
+}
+
+int32_t orc_lru_prefetch(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t* last_use, int32_t step,
+                         int32_t n, const int32_t* experts, int32_t max_prefetch, int32_t* admitted,
+                         int32_t* evicted) {
+    int32_t* listed = (int32_t*)calloc((size_t)n_experts, sizeof(int32_t));
+    for (int32_t i = 0; i < n; ++i) listed[experts[i]] = 1;
+    int32_t n_adm = 0;
+    for (int32_t i = 0; i < n && n_adm < max_prefetch; ++i) {
+        const int32_t e = experts[i];
+        int32_t resident = 0;
+        for (int32_t sl = 0; sl < C; ++sl)
+            if (slot_expert[sl] == e) resident = 1;
+        if (resident) continue;
+        int32_t victim = -1;
+        for (int32_t sl = 0; sl < C; ++sl) {
+            if (last_use[sl] == step) continue;
+            if (slot_expert[sl] >= 0 && listed[slot_expert[sl]]) continue;
+            if (victim < 0 || last_use[sl] < last_use[victim] ||
+                (last_use[sl] == last_use[victim] && slot_expert[sl] < slot_expert[victim]))
+                victim = sl;
+        }
+        if (victim < 0) break;
+        admitted[n_adm] = e;
+        evicted[n_adm] = slot_expert[victim];
+        ++n_adm;
+        slot_expert[victim] = e;
+        last_use[victim] = step;
+    }
+    free(listed);
     return n_adm;
 }

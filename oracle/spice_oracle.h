@@ -18,6 +18,8 @@
  *   LoRE     A   [r][d],  B [d][r]          (Eq. 9)
  * Slot id of token t's k-th routed choice = t*K + k.
  * Parity pins: see tests/test_oracle_*.py.  No function here is unpinned.
+ * Speculative prefetching (Alg. 1) uses an identity stand-in for the target layer's
+ * attention: this oracle covers the MoE part of the draft update only.
  */
 #ifndef SPICE_ORACLE_H
 #define SPICE_ORACLE_H
@@ -102,6 +104,50 @@ int32_t orc_exact_residual(const orc_cfg_t* c, int32_t T, const void* x, const i
 int32_t orc_lru_step(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t* last_use,
                      int32_t step, int32_t T, int32_t K, const int32_t* idx, const uint8_t* cls,
                      int32_t max_admit, int32_t* admitted, int32_t* evicted);
+
+/* ---- Speculative prefetching (Sec. 4.1, Eq. 2-5, Alg. 1) ----------------------------- */
+
+/* A value rounded to the storage dtype: nearest representable fp32 or bf16, ties to even
+ * (bf16 rounding is done once, from the double, not through fp32). */
+double orc_round_to(int32_t dtype, double v);
+
+/* One depth delta (1-based) of the draft rollout of Alg. 1 for T tokens, each token on
+ * its own.  Layer weights are those of layer l + delta: router wg[N][d] (+ bias[N] or
+ * NULL), shared block w13s/w2s, LoRE tables lA/lB [N] (every routed expert non-NULL when
+ * lore_rank > 0).  For a token still running (halted[t] == 0):
+ *   pi = softmax of the router logits of h_in[t] (Eq. 1); S = TopK(pi) (Eq. 2, ties to the
+ *   lower id); the prediction is enqueued: pred_idx[t][k] = S[k], pred_prob[t][k] = pi[S[k]];
+ *   conf[t] = sum_k pi[S[k]] (Eq. 5);
+ *   if delta >= l_min and conf[t] < tau: halted[t] = 1 (the prediction stays queued);
+ *   else unless last: h_out[t] = round(h_in[t] + sum_k pi_k (S(h_in[t]) + B_k A_k h_in[t]))
+ *   (the attention of the target layer is the identity here; Ẽ_k = S + B_k A_k, Eq. 11).
+ * A token halted before this depth gets pred_idx -1, pred_prob 0 and conf NaN.  h_out of
+ * a token not updated is h_in.  h_in and h_out are [T][d] in the cfg's dtype and may be
+ * the same array.  Returns 0, or -1 if a needed LoRE pointer is NULL. */
+int32_t orc_spec_step(const orc_cfg_t* c, int32_t T, int32_t delta, int32_t l_min, double tau, int32_t last,
+                      const void* h_in, const void* wg, const float* bias, const void* w13s, const void* w2s,
+                      const void* const* lA, const void* const* lB, int32_t* halted, int32_t* pred_idx,
+                      double* pred_prob, double* conf, void* h_out);
+
+/* Eq. 4: the least lookahead that hides the transfer of P experts of M_e bytes at
+ * bandwidth B behind per-layer compute T_attn + K T_expert:
+ * ceil(P M_e / (B (T_attn + K T_expert))).  Returns -1 if the compute window or B is not > 0. */
+int32_t orc_h_min(double P, double M_e, double B, double t_attn, int32_t K, double t_expert);
+
+/* Prefetch intents of one rollout (Eq. 3), per depth: the union over tokens of the
+ * enqueued sets, in issue order: larger predicted mass sum_t pi first, ties to the lower
+ * id; at most max_per_depth per depth.  pred_idx/pred_prob: [n_depth][T][K] as written
+ * by orc_spec_step (-1 = nothing enqueued).  experts [n_depth][max_per_depth], counts [n_depth]. */
+void orc_prefetch_queue(int32_t n_experts, int32_t n_depth, int32_t T, int32_t K, const int32_t* pred_idx,
+                        const double* pred_prob, int32_t max_per_depth, int32_t* experts, int32_t* counts);
+
+/* Speculative admissions into one layer's LRU cache at step `step`: the listed experts in
+ * order, skipping resident ones, each into the slot of the resident expert with the
+ * smallest (last_use, id) that was not used in this step and is not listed; the admitted
+ * expert gets last_use = step.  At most max_prefetch; returns the number admitted. */
+int32_t orc_lru_prefetch(int32_t n_experts, int32_t C, int32_t* slot_expert, int32_t* last_use, int32_t step,
+                         int32_t n, const int32_t* experts, int32_t max_prefetch, int32_t* admitted,
+                         int32_t* evicted);
 
 #ifdef __cplusplus
 }
