@@ -352,6 +352,88 @@ spice_status_t moe_expert_ffn_fetched(const spice_moe_cfg_t* cfg, int32_t T, con
                                       const void* w13_fetch, const void* w2_fetch, int32_t n_slots,
                                       float* y_slots, void* ws, size_t ws_bytes, spice_stream_t stream);
 
+/*
+ * Speculative prefetching (Sec. 4.1, Eq. 2-5, Alg. 1).  A draft rollout starts from the
+ * current layer's input hidden state h0 [T][d] and runs depth delta = 1, 2, ... with the
+ * weights of layer l + delta.  Each depth is three calls on one stream:
+ *   1. moe_route_bucket on the draft state with the future layer's router, every expert
+ *      absent (resident_slot all -1), conf all 0, cfg->conf_mode SPICE_CONF_INPUT,
+ *      cfg->norm_topk 0 and cfg->tau > 0: every slot is then LoRE and topk_w holds the
+ *      router's own probabilities pi;
+ *   2. moe_expert_ffn_grouped with that layer's shared block and LoRE factors (no hits):
+ *      y_shared = S(h), y_slots = B_k A_k h at each slot's bucket position;
+ *   3. moe_spec_update below.
+ * A token runs Alg. 1 on its own: it halts after the first depth >= l_min whose
+ * confidence is below tau.  The target layer's attention is not part of this library:
+ * the draft state moves by the MoE part only (an identity stand-in for Attn).
+ */
+
+/* Pinned host copies of one depth's predictions (each pointer may be NULL). */
+typedef struct {
+    int32_t* pred_idx;  /* [T][K] */
+    float* pred_prob;   /* [T][K] */
+    float* conf;        /* [T] */
+} spice_spec_host_t;
+
+/*
+ * Steps 2-4 of Alg. 1 at depth `depth` (1-based) for every token t with halted[t] == 0:
+ *   enqueue pred_idx[t][k] = topk_idx[t][k], pred_prob[t][k] = topk_w[t][k] (Eq. 2);
+ *   conf[t] = sum_k topk_w[t][k] (Eq. 5, summed in fp64, stored fp32);
+ *   if depth >= l_min and conf[t] < tau: halted[t] = 1;
+ *   else, unless last != 0: h_out[t] = h_in[t] + sum_k pi_k (y_shared[t] + y_slots[inv_perm[t*K+k]])
+ *   computed in fp32 and stored in the cfg's dtype (bf16: round to nearest even).
+ * Tokens halted before this depth get pred_idx -1, pred_prob 0, conf NaN; tokens not
+ * updated get h_out = h_in.
+ *   h_in, h_out  device [T][d] (dtype); h_out may be h_in itself but not overlap it otherwise
+ *   topk_idx, topk_w, inv_perm, y_slots, y_shared  device, from steps 1-2 of this depth
+ *                (y_slots is not read when cfg->lore_rank is 0)
+ *   halted       device [T] int32, in/out; zero it before depth 1
+ *   pred_idx, pred_prob, conf  device [T][K], [T][K], [T] out
+ *   host_out     nullable; pinned host copies written by the kernel (valid once the stream
+ *                has passed the call)
+ *   ws, ws_bytes the workspace of steps 1-2 (its flags word records an out-of-range inv_perm)
+ */
+spice_status_t moe_spec_update(const spice_moe_cfg_t* cfg, int32_t T, int32_t depth, int32_t l_min, float tau,
+                               int32_t last, const void* h_in, void* h_out, const int32_t* topk_idx,
+                               const float* topk_w, const int32_t* inv_perm, const float* y_slots,
+                               const float* y_shared, int32_t* halted, int32_t* pred_idx, float* pred_prob,
+                               float* conf, const spice_spec_host_t* host_out, void* ws, size_t ws_bytes,
+                               spice_stream_t stream);
+
+/*
+ * Eq. 4: the least lookahead depth that hides the copies of P experts of expert_bytes
+ * each at pcie_bytes_per_s behind per-layer compute t_attn_s + K * t_expert_s:
+ * ceil(P * expert_bytes / (pcie_bytes_per_s * (t_attn_s + K * t_expert_s))).
+ * Returns -1 if the compute window or the bandwidth is not > 0, or an argument is negative.
+ */
+int32_t moe_prefetch_h_min(double P, double expert_bytes, double pcie_bytes_per_s, double t_attn_s, int32_t K,
+                           double t_expert_s);
+
+/*
+ * The prefetch intents of one rollout (Eq. 3) as per-depth issue lists: the union over
+ * tokens of the experts enqueued at that depth, larger predicted mass sum_t pi first
+ * (summed in fp64), ties to the lower id, at most max_per_depth each.
+ *   pred_idx_host, pred_prob_host  host [n_depth][T][K] (-1 = nothing enqueued)
+ *   experts      host [n_depth][max_per_depth] out;  counts  host [n_depth] out
+ */
+spice_status_t moe_prefetch_queue(const spice_moe_cfg_t* cfg, int32_t T, int32_t n_depth,
+                                  const int32_t* pred_idx_host, const float* pred_prob_host, int32_t max_per_depth,
+                                  int32_t* experts, int32_t* counts);
+
+/*
+ * Speculative admissions into layer `layer`'s cache at decode step `step` (the bounded
+ * prefetch queue of Sec. 4.1): the n listed experts in order, skipping resident ones,
+ * each into the slot of the resident expert with the smallest (last_use, id) that was
+ * not used in this step and is not listed; the admitted expert gets last_use = step.
+ * At most max_prefetch.  Copies, ordering and moe_cache_wait work as for moe_cache_step
+ * (the copies go behind any admissions already queued on copy_stream).
+ *   admitted, evicted  host [max_prefetch] out, n_admitted out
+ */
+spice_status_t moe_cache_prefetch(spice_cache_t* cache, int32_t layer, int32_t step, int32_t n,
+                                  const int32_t* experts, int32_t max_prefetch, spice_stream_t copy_stream,
+                                  spice_stream_t compute_stream, int32_t* n_admitted, int32_t* admitted,
+                                  int32_t* evicted);
+
 /* Text of a status code, and the last error message of the calling thread. */
 const char* spice_status_string(spice_status_t status);
 const char* spice_last_error(void);

@@ -13,6 +13,13 @@
 //   - at most max_admit admissions per call (a bounded copy queue, Sec. 4.1).
 // The admitted experts are still served on the CPU at step s and are resident
 // for the layer's next call.
+// Speculative admissions (moe_cache_prefetch, Sec. 4.1) put predicted experts of a
+// future layer into that layer's least recently used slots that hold neither an
+// expert used at s nor another predicted one, ahead of the layer's call.
+//
+// Every batch of copies for a layer re-stages the layer's whole slot table from one
+// row of a small ring of pinned rows; batches of one layer are chained on the copy
+// streams, so the last batch's event covers them all.
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
@@ -41,7 +48,11 @@ struct spice_cache {
     std::vector<int32_t> last_use;               // [L*C], -1 = never
     std::vector<hipEvent_t> used, ready;         // per layer
     std::vector<uint8_t> pending;                // per layer: copies in flight
-    int32_t* resident_stage = nullptr;           // pinned [L*N], source of resident_slot updates
+    static constexpr int kRing = 4;              // staging rows per layer
+    int32_t* resident_stage = nullptr;           // pinned [L*kRing*N], sources of resident_slot updates
+    std::vector<hipEvent_t> stage_ev;            // [L*kRing]: the row's copy has been read
+    std::vector<uint8_t> stage_busy;             // [L*kRing]
+    std::vector<int32_t> stage_next;             // [L]
 };
 
 namespace {
@@ -58,17 +69,57 @@ void release(spice_cache* c) {
         if (e) (void)hipEventDestroy(e);
     for (hipEvent_t e : c->ready)
         if (e) (void)hipEventDestroy(e);
+    for (hipEvent_t e : c->stage_ev)
+        if (e) (void)hipEventDestroy(e);
     if (c->resident_stage) (void)hipHostFree(c->resident_stage);
     delete c;
 }
 
-// Fill the layer's staging row with the slot of every expert (-1 if absent).
-void stage_resident(spice_cache* c, int32_t l) {
-    int32_t* row = c->resident_stage + (size_t)l * c->N;
+// Fill staging row r of layer l with the slot of every expert (-1 if absent).
+int32_t* stage_resident(spice_cache* c, int32_t l, int32_t r) {
+    int32_t* row = c->resident_stage + ((size_t)l * spice_cache::kRing + r) * c->N;
     std::fill(row, row + c->N, -1);
     const int32_t* se = &c->slot_expert[(size_t)l * c->C];
     for (int32_t s = 0; s < c->C; ++s)
         if (se[s] >= 0) row[se[s]] = s;
+    return row;
+}
+
+struct Move {
+    int32_t expert, slot, old;
+};
+
+// Queue the copies of one batch of moves of layer l (state already updated): after the
+// work queued so far on compute_stream and after the layer's previous batch, the
+// weights into their slots, then the layer's slot table from a free staging row.
+hipError_t queue_moves(spice_cache* c, int32_t l, const std::vector<Move>& moves, hipStream_t copy_stream,
+                       hipStream_t compute_stream) {
+    const int32_t N = c->N;
+    const int32_t r = c->stage_next[l];
+    c->stage_next[l] = (r + 1) % spice_cache::kRing;
+    const size_t ri = (size_t)l * spice_cache::kRing + r;
+    hipError_t e = hipSuccess;
+    if (c->stage_busy[ri]) e = hipEventSynchronize(c->stage_ev[ri]);  // the row's last copy has run
+    c->stage_busy[ri] = 0;
+    if (e == hipSuccess) e = hipEventRecord(c->used[l], compute_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(copy_stream, c->used[l], 0);
+    if (e == hipSuccess && c->pending[l]) e = hipStreamWaitEvent(copy_stream, c->ready[l], 0);
+    for (size_t i = 0; i < moves.size() && e == hipSuccess; ++i) {
+        const Move& m = moves[i];
+        e = hipMemcpyAsync(static_cast<char*>(c->w13_pool[l]) + (size_t)m.slot * c->bytes13,
+                           c->w13_host[(size_t)l * N + m.expert], c->bytes13, hipMemcpyHostToDevice, copy_stream);
+        if (e == hipSuccess)
+            e = hipMemcpyAsync(static_cast<char*>(c->w2_pool[l]) + (size_t)m.slot * c->bytes2,
+                               c->w2_host[(size_t)l * N + m.expert], c->bytes2, hipMemcpyHostToDevice, copy_stream);
+    }
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(c->resident_dev[l], stage_resident(c, l, r), (size_t)N * 4, hipMemcpyHostToDevice,
+                           copy_stream);
+    if (e == hipSuccess) e = hipEventRecord(c->stage_ev[ri], copy_stream);
+    if (e == hipSuccess) c->stage_busy[ri] = 1;
+    if (e == hipSuccess) e = hipEventRecord(c->ready[l], copy_stream);
+    if (e == hipSuccess) c->pending[l] = 1;
+    return e;
 }
 
 }  // namespace
@@ -127,7 +178,8 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
                     release(c);
                     return err(SPICE_ERR_INVALID, "moe_cache_create: a pool or resident_slot pointer is NULL");
                 }
-            hipError_t e = hipHostMalloc((void**)&c->resident_stage, ln * sizeof(int32_t), hipHostMallocDefault);
+            hipError_t e = hipHostMalloc((void**)&c->resident_stage, ln * spice_cache::kRing * sizeof(int32_t),
+                                         hipHostMallocDefault);
             if (e != hipSuccess) {
                 c->resident_stage = nullptr;
                 release(c);
@@ -135,10 +187,15 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
             }
             c->used.assign((size_t)n_layers, nullptr);
             c->ready.assign((size_t)n_layers, nullptr);
+            c->stage_ev.assign((size_t)n_layers * spice_cache::kRing, nullptr);
+            c->stage_busy.assign((size_t)n_layers * spice_cache::kRing, 0);
+            c->stage_next.assign((size_t)n_layers, 0);
             for (int32_t l = 0; l < n_layers && e == hipSuccess; ++l) {
                 e = hipEventCreateWithFlags(&c->used[l], hipEventDisableTiming);
                 if (e == hipSuccess) e = hipEventCreateWithFlags(&c->ready[l], hipEventDisableTiming);
             }
+            for (size_t i = 0; i < c->stage_ev.size() && e == hipSuccess; ++i)
+                e = hipEventCreateWithFlags(&c->stage_ev[i], hipEventDisableTiming);
             if (e != hipSuccess) {
                 release(c);
                 return hip_err(e, "moe_cache_create: hipEventCreate");
@@ -161,11 +218,9 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
                             e = hipMemcpyAsync(static_cast<char*>(c->w2_pool[l]) + (size_t)s * c->bytes2, h2,
                                                c->bytes2, hipMemcpyHostToDevice, stream);
                     }
-                    if (e == hipSuccess) {
-                        stage_resident(c, l);
-                        e = hipMemcpyAsync(c->resident_dev[l], c->resident_stage + (size_t)l * N, (size_t)N * 4,
+                    if (e == hipSuccess)  // row 0; the load waits for the stream before returning
+                        e = hipMemcpyAsync(c->resident_dev[l], stage_resident(c, l, 0), (size_t)N * 4,
                                            hipMemcpyHostToDevice, stream);
-                    }
                 }
                 if (e == hipSuccess) e = hipStreamSynchronize(stream);
                 if (e != hipSuccess) {
@@ -228,9 +283,6 @@ spice_status_t moe_cache_step(spice_cache_t* c, int32_t layer, int32_t step, int
             if (slot_class_host[i] == SPICE_CLASS_HIT && where[topk_idx_host[i]] >= 0)
                 lu[where[topk_idx_host[i]]] = step;
 
-        struct Move {
-            int32_t expert, slot, old;
-        };
         std::vector<Move> moves;
         while ((int32_t)moves.size() < max_admit) {
             // candidate: an EXACT expert not resident right now, most slots first, then lower id
@@ -264,33 +316,64 @@ spice_status_t moe_cache_step(spice_cache_t* c, int32_t layer, int32_t step, int
         // The evicted slots are not read by this call's kernels (their experts were
         // not used at `step`), but resident_slot is: order the copies after the
         // call's work on the compute stream.
-        hipError_t e = hipSuccess;
-        if (c->pending[layer]) e = hipEventSynchronize(c->ready[layer]);  // staging row free again
-        if (e == hipSuccess) e = hipEventRecord(c->used[layer], compute_stream);
-        if (e == hipSuccess) e = hipStreamWaitEvent(copy_stream, c->used[layer], 0);
-        for (size_t i = 0; i < moves.size() && e == hipSuccess; ++i) {
-            const Move& m = moves[i];
-            e = hipMemcpyAsync(static_cast<char*>(c->w13_pool[layer]) + (size_t)m.slot * c->bytes13,
-                               c->w13_host[(size_t)layer * N + m.expert], c->bytes13, hipMemcpyHostToDevice,
-                               copy_stream);
-            if (e == hipSuccess)
-                e = hipMemcpyAsync(static_cast<char*>(c->w2_pool[layer]) + (size_t)m.slot * c->bytes2,
-                                   c->w2_host[(size_t)layer * N + m.expert], c->bytes2, hipMemcpyHostToDevice,
-                                   copy_stream);
-        }
-        if (e == hipSuccess) {
-            stage_resident(c, layer);
-            e = hipMemcpyAsync(c->resident_dev[layer], c->resident_stage + (size_t)layer * N, (size_t)N * 4,
-                               hipMemcpyHostToDevice, copy_stream);
-        }
-        if (e == hipSuccess) e = hipEventRecord(c->ready[layer], copy_stream);
-        if (e != hipSuccess) return hip_err(e, "moe_cache_step");
-        c->pending[layer] = 1;
-        return SPICE_OK;
+        const hipError_t e = queue_moves(c, layer, moves, copy_stream, compute_stream);
+        return e == hipSuccess ? SPICE_OK : hip_err(e, "moe_cache_step");
     } catch (const std::exception& ex) {
         return err(SPICE_ERR_INTERNAL, std::string("moe_cache_step: ") + ex.what());
     } catch (...) {
         return err(SPICE_ERR_INTERNAL, "moe_cache_step: unknown exception");
+    }
+}
+
+spice_status_t moe_cache_prefetch(spice_cache_t* c, int32_t layer, int32_t step, int32_t n, const int32_t* experts,
+                                  int32_t max_prefetch, spice_stream_t copy_stream, spice_stream_t compute_stream,
+                                  int32_t* n_admitted, int32_t* admitted, int32_t* evicted) {
+    try {
+        if (!c) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: cache is NULL");
+        if (!n_admitted) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: n_admitted is NULL");
+        *n_admitted = 0;
+        if (layer < 0 || layer >= c->L) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: layer out of range");
+        if (step < 0) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: step must be >= 0");
+        if (n < 0 || max_prefetch < 0) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: n and max_prefetch must be >= 0");
+        if (n > 0 && !experts) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: experts is NULL");
+        if (max_prefetch > 0 && (!admitted || !evicted))
+            return err(SPICE_ERR_INVALID, "moe_cache_prefetch: admitted / evicted is NULL");
+        const int32_t N = c->N, C = c->C;
+        std::vector<uint8_t> listed((size_t)N, 0);
+        for (int32_t i = 0; i < n; ++i) {
+            if (experts[i] < 0 || experts[i] >= N) return err(SPICE_ERR_INVALID, "moe_cache_prefetch: expert id out of range");
+            listed[experts[i]] = 1;
+        }
+        int32_t* se = &c->slot_expert[(size_t)layer * C];
+        int32_t* lu = &c->last_use[(size_t)layer * C];
+        std::vector<Move> moves;
+        for (int32_t i = 0; i < n && (int32_t)moves.size() < max_prefetch; ++i) {
+            const int32_t e = experts[i];
+            if (std::find(se, se + C, e) != se + C) continue;  // already resident
+            if (c->device && (!c->w13_host[(size_t)layer * N + e] || !c->w2_host[(size_t)layer * N + e]))
+                continue;  // no host weights to copy from: not a prefetch candidate
+            int32_t v = -1;  // oldest use, then lower expert id (empty first); not used at `step`, not listed
+            for (int32_t s = 0; s < C; ++s) {
+                if (lu[s] == step || (se[s] >= 0 && listed[se[s]])) continue;
+                if (v < 0 || lu[s] < lu[v] || (lu[s] == lu[v] && se[s] < se[v])) v = s;
+            }
+            if (v < 0) break;
+            moves.push_back({e, v, se[v]});
+            se[v] = e;
+            lu[v] = step;
+        }
+        for (size_t i = 0; i < moves.size(); ++i) {
+            admitted[i] = moves[i].expert;
+            evicted[i] = moves[i].old;
+        }
+        *n_admitted = (int32_t)moves.size();
+        if (!c->device || moves.empty()) return SPICE_OK;
+        const hipError_t e = queue_moves(c, layer, moves, copy_stream, compute_stream);
+        return e == hipSuccess ? SPICE_OK : hip_err(e, "moe_cache_prefetch");
+    } catch (const std::exception& ex) {
+        return err(SPICE_ERR_INTERNAL, std::string("moe_cache_prefetch: ") + ex.what());
+    } catch (...) {
+        return err(SPICE_ERR_INTERNAL, "moe_cache_prefetch: unknown exception");
     }
 }
 

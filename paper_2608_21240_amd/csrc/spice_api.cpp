@@ -339,6 +339,63 @@ spice_status_t moe_expert_ffn_fetched(const spice_moe_cfg_t* cfg, int32_t T, con
     SPICE_TRY_END
 }
 
+spice_status_t moe_spec_update(const spice_moe_cfg_t* cfg, int32_t T, int32_t depth, int32_t l_min, float tau,
+                               int32_t last, const void* h_in, void* h_out, const int32_t* topk_idx,
+                               const float* topk_w, const int32_t* inv_perm, const float* y_slots,
+                               const float* y_shared, int32_t* halted, int32_t* pred_idx, float* pred_prob,
+                               float* conf, const spice_spec_host_t* host_out, void* ws, size_t ws_bytes,
+                               spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    spice_status_t st = check_cfg(cfg);
+    if (st != SPICE_OK) return st;
+    const spice_moe_cfg_t& c = *cfg;
+    if ((st = check_tokens(c, T)) != SPICE_OK) return st;
+    if (depth < 1) return fail(SPICE_ERR_INVALID, "moe_spec_update: depth must be >= 1");
+    if (l_min < 0) return fail(SPICE_ERR_INVALID, "moe_spec_update: l_min must be >= 0");
+    if (!(tau >= 0.f) || std::isinf(tau)) return fail(SPICE_ERR_INVALID, "moe_spec_update: tau must be finite and >= 0");
+    if (T == 0) return SPICE_OK;
+    SPICE_REQUIRE(h_in, "h_in");
+    SPICE_REQUIRE(h_out, "h_out");
+    SPICE_REQUIRE(topk_idx, "topk_idx");
+    SPICE_REQUIRE(topk_w, "topk_w");
+    SPICE_REQUIRE(inv_perm, "inv_perm");
+    SPICE_REQUIRE(y_shared, "y_shared");
+    if (c.lore_rank > 0) SPICE_REQUIRE(y_slots, "y_slots");
+    SPICE_REQUIRE(halted, "halted");
+    SPICE_REQUIRE(pred_idx, "pred_idx");
+    SPICE_REQUIRE(pred_prob, "pred_prob");
+    SPICE_REQUIRE(conf, "conf");
+    if ((st = check_ws(c, T, ws, ws_bytes)) != SPICE_OK) return st;
+    const size_t hb = (size_t)T * c.d * elem_size(c);
+    if (h_out != h_in && overlaps(h_out, hb, h_in, hb))
+        return fail(SPICE_ERR_INVALID, "moe_spec_update: h_out overlaps h_in without being it");
+    spice::SpecArgs a{};
+    a.T = T; a.d = c.d; a.K = c.top_k; a.dtype = c.dtype; a.delta = depth; a.l_min = l_min;
+    a.last = last != 0; a.lore = c.lore_rank > 0; a.tau = tau;
+    a.h_in = h_in; a.h_out = h_out; a.topk_idx = topk_idx; a.topk_w = topk_w; a.inv_perm = inv_perm;
+    a.y_slots = y_slots; a.y_shared = y_shared; a.halted = halted; a.pred_idx = pred_idx;
+    a.pred_prob = pred_prob; a.conf = conf; a.ctrl = static_cast<uint32_t*>(ws);
+    if (host_out) {
+        void* d = nullptr;
+        if (host_out->pred_idx) {
+            if ((st = gpu_address(host_out->pred_idx, true, "host_out.pred_idx", &d)) != SPICE_OK) return st;
+            a.h_pred_idx = static_cast<int32_t*>(d);
+        }
+        if (host_out->pred_prob) {
+            if ((st = gpu_address(host_out->pred_prob, true, "host_out.pred_prob", &d)) != SPICE_OK) return st;
+            a.h_pred_prob = static_cast<float*>(d);
+        }
+        if (host_out->conf) {
+            if ((st = gpu_address(host_out->conf, true, "host_out.conf", &d)) != SPICE_OK) return st;
+            a.h_conf = static_cast<float*>(d);
+        }
+    }
+    const hipError_t e = spice::launch_spec_update(a, stream);
+    if (e != hipSuccess) return hip_fail(e, "moe_spec_update");
+    return SPICE_OK;
+    SPICE_TRY_END
+}
+
 spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w, const uint8_t* slot_class,
                            const int32_t* inv_perm, const float* y_slots, const float* y_shared, const float* resid,
                            void* out, spice_stream_t stream) {

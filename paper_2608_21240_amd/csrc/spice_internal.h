@@ -99,6 +99,28 @@ struct FetchArgs {
     int32_t n_slots;
 };
 
+// One depth of the speculative-prefetch draft rollout (spec_draft.hip).
+struct SpecArgs {
+    int32_t T, d, K, dtype, delta, l_min, last, lore;
+    float tau;
+    const void* h_in;
+    void* h_out;            // may equal h_in
+    const int32_t* topk_idx;
+    const float* topk_w;
+    const int32_t* inv_perm;
+    const float* y_slots;
+    const float* y_shared;
+    int32_t* halted;        // [T], in/out
+    int32_t* pred_idx;      // [T][K]
+    float* pred_prob;       // [T][K]
+    float* conf;            // [T]
+    uint32_t* ctrl;
+    // device-visible addresses of the caller's pinned host copies (each nullable)
+    int32_t* h_pred_idx;
+    float* h_pred_prob;
+    float* h_conf;
+};
+
 struct CombineArgs {
     int32_t T, d, K, dtype;
     const float* topk_w;
@@ -140,6 +162,7 @@ hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn_fetched(const FfnArgs& a, const FetchArgs& f, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
+hipError_t launch_spec_update(const SpecArgs& a, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, size_t words, uint32_t value, hipStream_t s);
 
 }  // namespace spice

@@ -30,6 +30,7 @@ EXPORTS = (
     "moe_route_bucket", "moe_expert_ffn_grouped", "lore_surrogate_apply", "moe_combine",
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
     "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
+    "moe_spec_update", "moe_prefetch_h_min", "moe_prefetch_queue", "moe_cache_prefetch",
     "spice_status_string", "spice_last_error",
 )
 
@@ -51,6 +52,10 @@ class spice_split_cost_t(ctypes.Structure):
     _fields_ = [("cpu_bytes_per_s", ctypes.c_double), ("cpu_flops_per_s", ctypes.c_double),
                 ("pcie_bytes_per_s", ctypes.c_double), ("gpu_fixed_s", ctypes.c_double),
                 ("margin", ctypes.c_double)]
+
+
+class spice_spec_host_t(ctypes.Structure):
+    _fields_ = [("pred_idx", ctypes.c_void_p), ("pred_prob", ctypes.c_void_p), ("conf", ctypes.c_void_p)]
 
 
 class spice_host_out_t(ctypes.Structure):
@@ -99,6 +104,12 @@ def lib() -> ctypes.CDLL:
                                     ctypes.POINTER(_I)]),
             "moe_fetch_experts": (_I, [C, _I, _P, _P, _P, _P, _P, _I, _P, _P, _P]),
             "moe_expert_ffn_fetched": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I, _P, _P, _Z, _P]),
+            "moe_spec_update": (_I, [C, _I, _I, _I, ctypes.c_float, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
+                                     ctypes.POINTER(spice_spec_host_t), _P, _Z, _P]),
+            "moe_prefetch_h_min": (_I, [ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double, _I,
+                                        ctypes.c_double]),
+            "moe_prefetch_queue": (_I, [C, _I, _I, _P, _P, _I, _P, _P]),
+            "moe_cache_prefetch": (_I, [_P, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
             "spice_status_string": (ctypes.c_char_p, [_I]),
             "spice_last_error": (ctypes.c_char_p, []),
         }
@@ -249,6 +260,21 @@ class ExpertCache:
             adm.ctypes.data, ev.ctypes.data))
         return adm[:n.value].tolist(), ev[:n.value].tolist()
 
+    def prefetch(self, layer: int, step: int, experts, max_prefetch: int, copy_stream=None, compute_stream=None):
+        """Speculative admissions of the listed experts (issue order) -> (admitted, evicted)."""
+        import numpy as np
+
+        ex = np.ascontiguousarray(experts, dtype=np.int32).reshape(-1)
+        n = ctypes.c_int32(0)
+        adm = np.empty(max(max_prefetch, 1), np.int32)
+        ev = np.empty(max(max_prefetch, 1), np.int32)
+        dev = self.device
+        _check("moe_cache_prefetch", lib().moe_cache_prefetch(
+            self.h, layer, step, ex.size, ex.ctypes.data if ex.size else None, max_prefetch,
+            _stream(copy_stream) if dev else None, _stream(compute_stream) if dev else None, ctypes.byref(n),
+            adm.ctypes.data, ev.ctypes.data))
+        return adm[:n.value].tolist(), ev[:n.value].tolist()
+
     def wait(self, layer: int, stream=None) -> None:
         _check("moe_cache_wait", lib().moe_cache_wait(self.h, layer, _stream(stream)))
 
@@ -299,3 +325,35 @@ def moe_expert_ffn_fetched(cfg, T, x, perm, offsets, slot_class, fetch_expert, w
     _check("moe_expert_ffn_fetched", lib().moe_expert_ffn_fetched(
         ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(slot_class), _p(fetch_expert), _p(w13_fetch),
         _p(w2_fetch), n_slots, _p(y_slots), _p(ws), ws_bytes, _stream(stream)))
+
+
+def spec_host(pred_idx=None, pred_prob=None, conf=None) -> spice_spec_host_t:
+    """Pinned host copies of one depth's predictions (CPU tensors from pin_memory())."""
+    return spice_spec_host_t(_p(pred_idx), _p(pred_prob), _p(conf))
+
+
+def moe_spec_update(cfg, T, depth, l_min, tau, last, h_in, h_out, topk_idx, topk_w, inv_perm, y_slots, y_shared,
+                    halted, pred_idx, pred_prob, conf, host_out=None, ws=None, ws_bytes=0, stream=None) -> None:
+    _check("moe_spec_update", lib().moe_spec_update(
+        ctypes.byref(cfg), T, depth, l_min, tau, int(last), _p(h_in), _p(h_out), _p(topk_idx), _p(topk_w),
+        _p(inv_perm), _p(y_slots), _p(y_shared), _p(halted), _p(pred_idx), _p(pred_prob), _p(conf),
+        None if host_out is None else ctypes.byref(host_out), _p(ws), ws_bytes, _stream(stream)))
+
+
+def moe_prefetch_h_min(P, expert_bytes, pcie_bytes_per_s, t_attn_s, K, t_expert_s) -> int:
+    return lib().moe_prefetch_h_min(P, expert_bytes, pcie_bytes_per_s, t_attn_s, K, t_expert_s)
+
+
+def moe_prefetch_queue(cfg, pred_idx_host, pred_prob_host, max_per_depth: int):
+    """Per-depth issue lists from host predictions [n_depth][T][K]."""
+    import numpy as np
+
+    pidx = np.ascontiguousarray(pred_idx_host, dtype=np.int32)
+    pprob = np.ascontiguousarray(pred_prob_host, dtype=np.float32)
+    D, T = pidx.shape[0], pidx.shape[1]
+    ex = np.empty((D, max(max_per_depth, 1)), np.int32)
+    cnt = np.zeros(max(D, 1), np.int32)
+    _check("moe_prefetch_queue", lib().moe_prefetch_queue(
+        ctypes.byref(cfg), T, D, pidx.ctypes.data, pprob.ctypes.data, max_per_depth, ex.ctypes.data,
+        cnt.ctypes.data))
+    return [ex[i, :cnt[i]].tolist() for i in range(D)]

@@ -16,7 +16,7 @@ DUMMY = 0x1000  # never dereferenced: every case below fails validation first
 def declared_functions():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(?:spice_status_t|size_t|void|const char\*)\s+(\w+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(?:spice_status_t|size_t|int32_t|void|const char\*)\s+(\w+)\s*\(", text)))
 
 
 def test_every_declared_symbol_is_exported():
@@ -126,3 +126,30 @@ def test_pageable_host_copies_are_rejected():
         ho = spice.host_out(**{field: buf})
         assert route(cfg(), host_out=ho) == spice.SPICE_ERR_INVALID
         assert "host_out." + field in spice.last_error()
+
+
+def test_spec_update_validates_on_the_host():
+    L = spice.lib()
+    c = cfg()
+    D = DUMMY
+    ws = spice.spice_workspace_bytes(c, 4)
+
+    def call(T=4, depth=1, l_min=1, tau=0.5, h_in=D, h_out=D, **kw):
+        p = dict(topk_idx=D, topk_w=D, inv_perm=D, y_slots=D, y_shared=D, halted=D, pred_idx=D, pred_prob=D,
+                 conf=D, ws=D)
+        p.update(kw)
+        return L.moe_spec_update(ctypes.byref(c), T, depth, l_min, tau, 0, h_in, h_out, p["topk_idx"],
+                                 p["topk_w"], p["inv_perm"], p["y_slots"], p["y_shared"], p["halted"],
+                                 p["pred_idx"], p["pred_prob"], p["conf"], None, p["ws"], ws, None)
+
+    assert call(depth=0) == spice.SPICE_ERR_INVALID
+    assert call(l_min=-1) == spice.SPICE_ERR_INVALID
+    assert call(tau=float("nan")) == spice.SPICE_ERR_INVALID
+    assert call(tau=float("inf")) == spice.SPICE_ERR_INVALID
+    assert call(tau=-0.1) == spice.SPICE_ERR_INVALID
+    for k in ("topk_idx", "topk_w", "inv_perm", "y_shared", "halted", "pred_idx", "pred_prob", "conf"):
+        assert call(**{k: None}) == spice.SPICE_ERR_INVALID, k
+    assert call(h_in=None) == spice.SPICE_ERR_INVALID
+    assert call(h_out=D + 64) == spice.SPICE_ERR_INVALID  # overlaps h_in without being it
+    assert call(ws=None) == spice.SPICE_ERR_INVALID
+    assert call(T=0, depth=1) == spice.SPICE_OK
