@@ -247,9 +247,11 @@ class LayerRun:
 
     def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
                 exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None,
-                split=None):
+                split=None, after_experts=None):
         """One layer call: route, FFN + LoRE on the GPU overlapped with the exact CPU residual
-        (and, with a split cost model, the fetched exact misses on the GPU), combine."""
+        (and, with a split cost model, the fetched exact misses on the GPU), combine.
+        after_experts (callable) queues more GPU work right after the FFN, ahead of the host
+        residual, e.g. a speculative-prefetch rollout."""
         T = self.T if T is None else T
         ev = events or {}
         self.x_cur = x
@@ -263,6 +265,8 @@ class LayerRun:
         self.experts(L, x, T, fuse_lore=True)
         if "experts" in ev:
             ev["experts"].record()
+        if after_experts is not None:
+            after_experts()
         if exact:
             self.exact_host(L, T, n_threads, split)
         if "resid" in ev:

@@ -7,7 +7,7 @@ used by every layer; they do not change what the cache does, which depends on
 routing only.  Each step feeds one x[T][d] draw to every layer (the layers are
 not chained).  Per layer call: route, FFN + LoRE, exact residual on the host,
 combine (LayerRun.forward), then the cache update, whose copies overlap the
-following layers.
+following layers; optionally the speculative prefetches of the next layers.
 """
 from __future__ import annotations
 
@@ -71,11 +71,22 @@ class StackModel:
 
 
 class StackRun:
-    """Runs decode steps over the stack and records the cache's behaviour."""
+    """Runs decode steps over the stack and records the cache's behaviour.
 
-    def __init__(self, model: StackModel, max_admit: int = 4, n_threads: int = 0):
+    prefetch (optional): dict(depth, l_min, tau, max_prefetch) turns on speculative
+    prefetching (Sec. 4.1): after each layer's FFN the draft rollout of Alg. 1 runs from
+    the layer's input over the next `depth` layers (overlapped with the host residual),
+    and after the layer's own admissions the cache takes up to max_prefetch predicted
+    experts per future layer, in issue order, from lists cut at the cache size."""
+
+    def __init__(self, model: StackModel, max_admit: int = 4, n_threads: int = 0, prefetch: Optional[Dict] = None):
         wl, s = model.wl, model.shape
         self.m, self.max_admit, self.n_threads = model, max_admit, n_threads
+        self.prefetch = prefetch
+        self.spec = None
+        if prefetch:
+            from .spec import SpecRollout
+            self.spec = SpecRollout(s, wl.tokens, prefetch["depth"])
         self.T = wl.tokens
         self.run = LayerRun(s, self.T, model.C, tau=wl.tau, conf_mode=wl.conf_mode, norm_topk=wl.norm_topk)
         self.cfg = self.run.cfg
@@ -92,21 +103,33 @@ class StackRun:
     def step(self, step: int, x: torch.Tensor, confs: List[torch.Tensor], record: bool = True,
              outputs: Optional[Dict] = None) -> None:
         """One decode step through every layer.  outputs: {layer: tensor to copy the output into}."""
-        K = self.m.shape.top_k
-        for l in range(self.m.L):
+        K, L = self.m.shape.top_k, self.m.L
+        pf = self.prefetch
+        for l in range(L):
             self.cache.wait(l)
-            out = self.run.forward(self.views[l], x, confs[l], self.T, n_threads=self.n_threads)
+            future = self.views[l + 1: l + 1 + pf["depth"]] if pf else []
+            hook = (lambda: self.spec.run(future, x, pf["l_min"], pf["tau"])) if future else None
+            out = self.run.forward(self.views[l], x, confs[l], self.T, n_threads=self.n_threads, after_experts=hook)
             if outputs is not None and l in outputs:
                 outputs[l].copy_(out)
             idx = self.run.idx_host[: self.T].numpy()
             cls = self.run.cls_host[: self.T].numpy()
             adm, ev = self.cache.step(l, step, idx, cls, self.max_admit, copy_stream=self.copy_stream)
+            queue, pre = [], []
+            if future:
+                # issue lists truncated to the cache size: a prefetch never evicts one of the
+                # layer's C most likely experts to make room for another
+                queue = self.spec.queue(self.m.C)
+                for j, q in enumerate(queue):
+                    pre.append(self.cache.prefetch(l + 1 + j, step, q, pf["max_prefetch"],
+                                                   copy_stream=self.copy_stream))
             if record:
                 cnt = np.bincount(cls.ravel(), minlength=3)
                 self.trace.append(dict(step=step, layer=l, idx=idx.copy(), cls=cls.copy(), admitted=adm,
                                        evicted=ev, hit=int(cnt[0]), lore=int(cnt[1]), exact=int(cnt[2]),
                                        miss_rate=float(cnt[1] + cnt[2]) / (self.T * K),
-                                       lore_split=float(cnt[1]) / max(int(cnt[1] + cnt[2]), 1)))
+                                       lore_split=float(cnt[1]) / max(int(cnt[1] + cnt[2]), 1),
+                                       queue=queue, prefetched=pre))
 
     def close(self) -> None:
         torch.cuda.synchronize()

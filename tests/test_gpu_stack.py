@@ -91,3 +91,59 @@ def test_stack_lru_matches_oracle(orc):
     print(f"[stack] slot hit rate {hit_rate:.3f}, LoRE share of misses "
           f"{totals[LORE] / max(totals[LORE] + totals[EXACT], 1):.3f}, admissions {n_adm}", flush=True)
     assert n_adm > 0 and 0.1 < hit_rate < 0.9
+
+
+def test_stack_with_speculative_prefetch_matches_oracle(orc):
+    """The same stack with speculative prefetching (Sec. 4.1): after each layer, the draft
+    rollout's issue lists for the next two layers go into their caches (at most 3 per
+    layer).  The oracle replays every demand admission and every prefetch batch on its own
+    LRU state, and the classes of each call follow from that state.  The stack feeds the
+    same x to every layer, so a depth-1 prediction is the next layer's routing itself:
+    this checks the bookkeeping and measures the hit rate, not prediction quality."""
+    wl = WORKLOADS["dsv2_stack"]
+    s = wl.shape
+    L, T, N, C = wl.layers, wl.tokens, s.n_experts, wl.cache_slots
+    steps = 24
+    pf = dict(depth=2, l_min=1, tau=0.0, max_prefetch=3)
+    m = StackModel(wl)
+    ocfg = orc.make_cfg(s, tau=wl.tau)
+    rates = {}
+    for use in (False, True):
+        sr = StackRun(m, max_admit=4, prefetch=pf if use else None)  # loads the initial experts again
+        refs = [orc.LRUState(N, C, m.initial[l]) for l in range(L)]
+        totals = np.zeros(3, np.int64)
+        n_pre = 0
+        for step in range(steps):
+            x = to_tensor(synth.gen_x(wl, 0, step, T), s.dtype, "cuda")
+            conf_np = [synth.gen_conf(wl, l, step, T) for l in range(L)]
+            sr.step(step, x, [torch.from_numpy(c).cuda() for c in conf_np])
+            for l in range(L):
+                tr = sr.trace[step * L + l]
+                ocls = orc.classify(ocfg, tr["idx"], refs[l].resident_mask(), conf_np[l])
+                assert np.array_equal(ocls, tr["cls"]), (use, step, l)
+                a, e = refs[l].step(step, tr["idx"], tr["cls"], 4)
+                assert tr["admitted"] == a.tolist() and tr["evicted"] == e.tolist(), (use, step, l)
+                if use:
+                    assert len(tr["queue"]) == min(pf["depth"], L - 1 - l)
+                    for j, q in enumerate(tr["queue"]):
+                        pa, pe = refs[l + 1 + j].prefetch(step, q, pf["max_prefetch"])
+                        assert tr["prefetched"][j] == (pa.tolist(), pe.tolist()), (step, l, j)
+                        n_pre += len(pa)
+                totals += np.bincount(tr["cls"].ravel(), minlength=3)
+        torch.cuda.synchronize()
+        for l in range(L):
+            se, lu = sr.cache.state(l)
+            assert se.tolist() == refs[l].slot_expert.tolist() and lu.tolist() == refs[l].last_use.tolist(), l
+        # the pools hold what the cache says
+        for l in (1, L // 2, L - 1):
+            for slot in range(C):
+                e = int(refs[l].slot_expert[slot])
+                w13, w2 = m.host_storage(e)
+                assert np.array_equal(to_np(m.w13_pool[l][slot]), w13), (use, l, slot, e)
+            assert sr.spec is None or sr.spec.flags() == 0
+        sr.close()
+        rates[use] = (totals[HIT] / totals.sum(), totals[EXACT] / totals.sum(), n_pre)
+        print(f"[stack] prefetch={use}: slot hit rate {rates[use][0]:.3f}, exact share {rates[use][1]:.3f}, "
+              f"prefetched experts {n_pre}", flush=True)
+    assert rates[True][2] > 0 and rates[True][0] > rates[False][0]
+
