@@ -63,9 +63,13 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="finish with a plain device copy of this many MiB (a known-size reference for counters)")
-    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill"),
+    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill", "dsv2_stack"),
                    help="dsv2_decode: the decode layer (default); qwen2_prefill: the 4096-token "
-                        "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path")
+                        "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path; dsv2_stack: the 26-layer "
+                        "LRU-cached decode stack with and without speculative prefetching")
+    p.add_argument("--spec-depth", type=int, default=2, help="dsv2_stack: lookahead layers of the draft rollout")
+    p.add_argument("--spec-tau", type=float, default=0.0, help="dsv2_stack: halting threshold of the rollout")
+    p.add_argument("--max-prefetch", type=int, default=3, help="dsv2_stack: prefetched experts per layer and call")
     p.add_argument("--resident", type=int, default=64, help="qwen2_prefill: resident experts")
     p.add_argument("--split", default="auto", choices=("auto", "off"),
                    help="exact-miss split (Eq. 12): auto = calibrate the cost model on this host and let the "
@@ -122,6 +126,8 @@ def main():
     torch.cuda.set_device(0)
     if args.workload == "qwen2_prefill":
         return prefill_main(args)
+    if args.workload == "dsv2_stack":
+        return stack_main(args)
     batches = [int(b) for b in args.batches.split(",")]
     wl = W.WORKLOADS["dsv2_decode_t32"]
     shape = wl.shape
@@ -311,6 +317,86 @@ def calibrate_split(run, dev, shape, T, args):
     pcie = len(probe) * shape.expert_bytes / min(fetch_time(), fetch_time())
     # the GPU side pays one fetched-FFN call (two launches); a split must save 5 %
     return spice.spice_split_cost_t(cpu_bytes, cpu_flops, pcie, 30e-6, 0.05)
+
+
+def stack_main(args):
+    """26 DSV2-Lite-shaped layers with a 24-slot LRU cache each, T=64 per step (the stack
+    workload), run with and without speculative prefetching (Sec. 4.1).  Every step is a
+    whole decode step through all layers: per layer route, FFN + LoRE, the host residual of
+    the exact misses, combine, the cache's admissions and, with prefetching, the draft
+    rollout (overlapped with the host residual) and the speculative admissions.  The
+    roofline is for the rollout's own GPU work (route + shared/LoRE FFN + update per depth),
+    HBM-bound: router + shared block + distinct predicted experts' LoRE factors per depth."""
+    import torch
+
+    from paper_2608_21240_amd import synth, workloads as W
+    from paper_2608_21240_amd.layer import to_tensor
+    from paper_2608_21240_amd.stack import StackModel, StackRun
+
+    wl = W.WORKLOADS["dsv2_stack"]
+    s, T, L = wl.shape, wl.tokens, wl.layers
+    t_gen = time.time()
+    m = StackModel(wl)
+    print(f"[bench] stack of {L} layers ready in {time.time() - t_gen:.1f}s", file=sys.stderr, flush=True)
+    pf = dict(depth=args.spec_depth, l_min=1, tau=args.spec_tau, max_prefetch=args.max_prefetch)
+    xs = [to_tensor(synth.gen_x(wl, 0, k, T), s.dtype, "cuda") for k in range(args.warmup + args.steps)]
+    confs = [[torch.from_numpy(synth.gen_conf(wl, l, k, T)).cuda() for l in range(L)]
+             for k in range(args.warmup + args.steps)]
+    res = {}
+    for use in (False, True):
+        sr = StackRun(m, max_admit=4, prefetch=pf if use else None, n_threads=args.threads)
+        for k in range(args.warmup):
+            sr.step(k, xs[k], confs[k])
+        torch.cuda.synchronize()
+        n0 = len(sr.trace)
+        if use:
+            sr.spec_events = []
+        t0 = time.perf_counter()
+        for k in range(args.warmup, args.warmup + args.steps):
+            sr.step(k, xs[k], confs[k])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        tr = sr.trace[n0:]
+        cnt = np.sum([np.bincount(t["cls"].ravel(), minlength=3) for t in tr], axis=0)
+        r = dict(tokens_per_s=T * args.steps / wall, ms_per_step=1e3 * wall / args.steps,
+                 slot_hit_rate=float(cnt[0] / cnt.sum()), exact_share=float(cnt[2] / cnt.sum()),
+                 admissions_per_call=float(np.mean([len(t["admitted"]) for t in tr])))
+        if use:
+            ms = np.array([a.elapsed_time(b) for a, b, _ in sr.spec_events])
+            depths = np.array([n for _, _, n in sr.spec_events])
+            # algorithmic bytes of one depth: router, shared block, LoRE factors of the distinct
+            # predicted experts (from the issue lists, uncut), x/h rows and the fp32 outputs
+            wb = s.wbytes
+            nexp = [len(set(np.concatenate([sr.spec.pred_idx_h[j].numpy().ravel()]).tolist()) - {-1})
+                    for j in range(sr.spec.n)]
+            per_depth = (s.n_experts * s.d * wb + s.shared_bytes + float(np.mean(nexp)) * s.lore_bytes
+                         + 2 * T * s.d * wb + (T * s.top_k + T) * s.d * 4)
+            r.update(rollout_us=float(ms.mean() * 1e3), rollout_us_per_depth=float((ms / depths).mean() * 1e3),
+                     rollout_GBps=float(per_depth * depths.sum() / (ms.sum() * 1e-3) / 1e9),
+                     bytes_per_depth=int(per_depth),
+                     prefetched_per_call=float(np.mean([sum(len(a) for a, _ in t["prefetched"]) for t in tr])))
+        sr.close()
+        res["prefetch" if use else "no_prefetch"] = {k: (round(v, 4) if isinstance(v, float) else v)
+                                                     for k, v in r.items()}
+        print(f"[bench] stack prefetch={use}: {json.dumps(res['prefetch' if use else 'no_prefetch'])}",
+              file=sys.stderr, flush=True)
+    on = res["prefetch"]
+    line = {
+        "metric": "MoE stack decode tokens/s, 26 DSV2-Lite-shaped layers, 24-slot LRU cache per layer",
+        "value": round(on["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(on["ms_per_step"], 3), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded random-init DSV2-Lite-shaped layers, conf~U(0,1); every layer sees the same x)",
+        "config": {"workload": "dsv2_stack_T64_L26_C24_prefetch", "layers": L, "tokens": T,
+                   "cache_slots": wl.cache_slots, "max_admit": 4, "spec_depth": pf["depth"],
+                   "spec_tau": pf["tau"], "max_prefetch": pf["max_prefetch"]},
+        "roofline": {"bound": "hbm", "kernel": "draft rollout per depth: route + shared/LoRE FFN + spec update",
+                     "achieved": round(on["rollout_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(on["rollout_GBps"] / HBM_PEAK_GBS, 4), "traffic": None,
+                     "bytes_per_depth": on["bytes_per_depth"], "avg_depth_us": round(on["rollout_us_per_depth"], 2)},
+        "by_mode": res,
+    }
+    print(json.dumps(line), flush=True)
 
 
 MFMA_BF16_PEAK_TFLOPS = 2500.0

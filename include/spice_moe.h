@@ -269,7 +269,8 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
  *   topk_idx_host, slot_class_host  host [T][K]: the call's routing (moe_route_bucket)
  *   max_admit          admissions allowed in this call (>= 0)
  *   copy_stream        stream of the host -> pool copies; compute_stream: stream of the
- *                      layer's kernels (the copies wait for its queued work)
+ *                      layer's kernels (the copies wait for its queued work, which this
+ *                      call marks as the layer's last use on every call)
  *   n_admitted         out: number admitted
  *   admitted, evicted  host [max_admit] out: admitted experts in order, and the expert
  *                      each one replaced (-1 = the slot was empty)
@@ -425,8 +426,12 @@ spice_status_t moe_prefetch_queue(const spice_moe_cfg_t* cfg, int32_t T, int32_t
  * prefetch queue of Sec. 4.1): the n listed experts in order, skipping resident ones,
  * each into the slot of the resident expert with the smallest (last_use, id) that was
  * not used in this step and is not listed; the admitted expert gets last_use = step.
- * At most max_prefetch.  Copies, ordering and moe_cache_wait work as for moe_cache_step
- * (the copies go behind any admissions already queued on copy_stream).
+ * At most max_prefetch.  The copies wait for the layer's last call, as marked by its
+ * last moe_cache_step (so every call of a layer must be followed by moe_cache_step for
+ * it before a prefetch into it), and for the layer's earlier copies; they do not wait
+ * for other work on the compute stream, so a prefetch into a future layer overlaps the
+ * current one.  moe_cache_wait orders the layer's next call after them.  Experts whose
+ * host weights are NULL are skipped.  compute_stream is not used.
  *   admitted, evicted  host [max_prefetch] out, n_admitted out
  */
 spice_status_t moe_cache_prefetch(spice_cache_t* cache, int32_t layer, int32_t step, int32_t n,

@@ -46,8 +46,9 @@ struct spice_cache {
     std::vector<int32_t*> resident_dev;          // [L]
     std::vector<int32_t> slot_expert;            // [L*C], -1 = empty
     std::vector<int32_t> last_use;               // [L*C], -1 = never
-    std::vector<hipEvent_t> used, ready;         // per layer
+    std::vector<hipEvent_t> used, ready;         // per layer: its last call's work; its last copies
     std::vector<uint8_t> pending;                // per layer: copies in flight
+    std::vector<uint8_t> used_valid;             // per layer: `used` has been recorded
     static constexpr int kRing = 4;              // staging rows per layer
     int32_t* resident_stage = nullptr;           // pinned [L*kRing*N], sources of resident_slot updates
     std::vector<hipEvent_t> stage_ev;            // [L*kRing]: the row's copy has been read
@@ -90,10 +91,9 @@ struct Move {
 };
 
 // Queue the copies of one batch of moves of layer l (state already updated): after the
-// work queued so far on compute_stream and after the layer's previous batch, the
+// layer's last call (its `used` event) and after the layer's previous batch, the
 // weights into their slots, then the layer's slot table from a free staging row.
-hipError_t queue_moves(spice_cache* c, int32_t l, const std::vector<Move>& moves, hipStream_t copy_stream,
-                       hipStream_t compute_stream) {
+hipError_t queue_moves(spice_cache* c, int32_t l, const std::vector<Move>& moves, hipStream_t copy_stream) {
     const int32_t N = c->N;
     const int32_t r = c->stage_next[l];
     c->stage_next[l] = (r + 1) % spice_cache::kRing;
@@ -101,8 +101,7 @@ hipError_t queue_moves(spice_cache* c, int32_t l, const std::vector<Move>& moves
     hipError_t e = hipSuccess;
     if (c->stage_busy[ri]) e = hipEventSynchronize(c->stage_ev[ri]);  // the row's last copy has run
     c->stage_busy[ri] = 0;
-    if (e == hipSuccess) e = hipEventRecord(c->used[l], compute_stream);
-    if (e == hipSuccess) e = hipStreamWaitEvent(copy_stream, c->used[l], 0);
+    if (e == hipSuccess && c->used_valid[l]) e = hipStreamWaitEvent(copy_stream, c->used[l], 0);
     if (e == hipSuccess && c->pending[l]) e = hipStreamWaitEvent(copy_stream, c->ready[l], 0);
     for (size_t i = 0; i < moves.size() && e == hipSuccess; ++i) {
         const Move& m = moves[i];
@@ -166,6 +165,7 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
         c->slot_expert.assign(initial_experts, initial_experts + (size_t)n_layers * C);
         c->last_use.assign((size_t)n_layers * C, -1);
         c->pending.assign((size_t)n_layers, 0);
+        c->used_valid.assign((size_t)n_layers, 0);
         if (device) {
             const size_t ln = (size_t)n_layers * N;
             c->w13_host.assign(w13_host, w13_host + ln);
@@ -311,12 +311,15 @@ spice_status_t moe_cache_step(spice_cache_t* c, int32_t layer, int32_t step, int
             evicted[i] = moves[i].old;
         }
         *n_admitted = (int32_t)moves.size();
-        if (!c->device || moves.empty()) return SPICE_OK;
+        if (!c->device) return SPICE_OK;
 
-        // The evicted slots are not read by this call's kernels (their experts were
-        // not used at `step`), but resident_slot is: order the copies after the
-        // call's work on the compute stream.
-        const hipError_t e = queue_moves(c, layer, moves, copy_stream, compute_stream);
+        // The call's work on the compute stream is the layer's last use of its pools
+        // (marked on every call).  The evicted slots are not read by this call's kernels
+        // (their experts were not used at `step`), but resident_slot is: the copies go
+        // after that work.
+        hipError_t e = hipEventRecord(c->used[layer], compute_stream);
+        if (e == hipSuccess) c->used_valid[layer] = 1;
+        if (e == hipSuccess && !moves.empty()) e = queue_moves(c, layer, moves, copy_stream);
         return e == hipSuccess ? SPICE_OK : hip_err(e, "moe_cache_step");
     } catch (const std::exception& ex) {
         return err(SPICE_ERR_INTERNAL, std::string("moe_cache_step: ") + ex.what());
@@ -368,7 +371,10 @@ spice_status_t moe_cache_prefetch(spice_cache_t* c, int32_t layer, int32_t step,
         }
         *n_admitted = (int32_t)moves.size();
         if (!c->device || moves.empty()) return SPICE_OK;
-        const hipError_t e = queue_moves(c, layer, moves, copy_stream, compute_stream);
+        // the copies wait for the layer's last call (moe_cache_step's mark), not for
+        // whatever else the compute stream holds: a prefetch overlaps the current layer
+        (void)compute_stream;
+        const hipError_t e = queue_moves(c, layer, moves, copy_stream);
         return e == hipSuccess ? SPICE_OK : hip_err(e, "moe_cache_prefetch");
     } catch (const std::exception& ex) {
         return err(SPICE_ERR_INTERNAL, std::string("moe_cache_prefetch: ") + ex.what());

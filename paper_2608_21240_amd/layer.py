@@ -220,11 +220,13 @@ class LayerRun:
         spice.moe_combine(self.cfg, T, self.topk_w, self.slot_class, self.inv_perm, self.y_slots, self.y_shared,
                           resid, self.out)
 
-    def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0, split=None):
+    def exact_host(self, L: DeviceLayer, T: int, n_threads: int = 0, split=None, before_residual=None):
         """Wait for the route kernel's host copies; with a split cost model, fetch the experts
         the planner picks and queue their FFN on the GPU; then the CPU residual of the other
         exact misses into self.resid."""
         self.e_route.synchronize()
+        if before_residual is not None:
+            before_residual()
         self.last_fetch = []
         if split is not None and self.fetch_slots:
             cls = self.cls_host[:T].numpy()
@@ -247,11 +249,12 @@ class LayerRun:
 
     def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
                 exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None,
-                split=None, after_experts=None):
+                split=None, after_experts=None, before_residual=None):
         """One layer call: route, FFN + LoRE on the GPU overlapped with the exact CPU residual
         (and, with a split cost model, the fetched exact misses on the GPU), combine.
         after_experts (callable) queues more GPU work right after the FFN, ahead of the host
-        residual, e.g. a speculative-prefetch rollout."""
+        residual, e.g. a speculative-prefetch rollout; before_residual (callable) runs on the
+        host once the routing's host copies are there, just before the residual."""
         T = self.T if T is None else T
         ev = events or {}
         self.x_cur = x
@@ -268,7 +271,7 @@ class LayerRun:
         if after_experts is not None:
             after_experts()
         if exact:
-            self.exact_host(L, T, n_threads, split)
+            self.exact_host(L, T, n_threads, split, before_residual)
         if "resid" in ev:
             ev["resid"].record()
         self.combine(self.resid if exact else None, T)

@@ -55,7 +55,7 @@ class SpecRollout:
         self.pred_prob_h = torch.empty((depth, T, K), dtype=torch.float32).pin_memory()
         self.conf_h = torch.empty((depth, T), dtype=torch.float32).pin_memory()
         self.hosts = [spice.spec_host(self.pred_idx_h[j], self.pred_prob_h[j], self.conf_h[j]) for j in range(depth)]
-        self.done = torch.cuda.Event()
+        self.done = torch.cuda.Event(blocking=True)  # waiters sleep instead of spinning
         self.n, self.T_run = 0, T
 
     def state(self, j: int) -> torch.Tensor:

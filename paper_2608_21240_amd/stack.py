@@ -11,6 +11,7 @@ following layers; optionally the speculative prefetches of the next layers.
 """
 from __future__ import annotations
 
+import threading
 from types import SimpleNamespace
 from typing import Dict, List, Optional
 
@@ -84,6 +85,7 @@ class StackRun:
         self.m, self.max_admit, self.n_threads = model, max_admit, n_threads
         self.prefetch = prefetch
         self.spec = None
+        self.spec_events: Optional[List] = None  # set to [] to time every rollout
         if prefetch:
             from .spec import SpecRollout
             self.spec = SpecRollout(s, wl.tokens, prefetch["depth"])
@@ -108,21 +110,26 @@ class StackRun:
         for l in range(L):
             self.cache.wait(l)
             future = self.views[l + 1: l + 1 + pf["depth"]] if pf else []
-            hook = (lambda: self.spec.run(future, x, pf["l_min"], pf["tau"])) if future else None
-            out = self.run.forward(self.views[l], x, confs[l], self.T, n_threads=self.n_threads, after_experts=hook)
+            hook = (lambda: self._rollout(future, x)) if future else None
+            box: Dict = {}
+            helper = None
+            if future:
+                # the prefetches go out from a helper thread as soon as the rollout is done,
+                # while this thread computes the layer's host residual; their copies wait
+                # only for the future layers' own last calls, so they overlap this layer
+                helper = threading.Thread(target=self._issue_prefetch, args=(l, step, box))
+            out = self.run.forward(self.views[l], x, confs[l], self.T, n_threads=self.n_threads, after_experts=hook,
+                                   before_residual=helper.start if helper else None)
+            if helper is not None:
+                helper.join()
+                if "error" in box:
+                    raise box["error"]
             if outputs is not None and l in outputs:
                 outputs[l].copy_(out)
             idx = self.run.idx_host[: self.T].numpy()
             cls = self.run.cls_host[: self.T].numpy()
             adm, ev = self.cache.step(l, step, idx, cls, self.max_admit, copy_stream=self.copy_stream)
-            queue, pre = [], []
-            if future:
-                # issue lists truncated to the cache size: a prefetch never evicts one of the
-                # layer's C most likely experts to make room for another
-                queue = self.spec.queue(self.m.C)
-                for j, q in enumerate(queue):
-                    pre.append(self.cache.prefetch(l + 1 + j, step, q, pf["max_prefetch"],
-                                                   copy_stream=self.copy_stream))
+            queue, pre = box.get("queue", []), box.get("prefetched", [])
             if record:
                 cnt = np.bincount(cls.ravel(), minlength=3)
                 self.trace.append(dict(step=step, layer=l, idx=idx.copy(), cls=cls.copy(), admitted=adm,
@@ -130,6 +137,28 @@ class StackRun:
                                        miss_rate=float(cnt[1] + cnt[2]) / (self.T * K),
                                        lore_split=float(cnt[1]) / max(int(cnt[1] + cnt[2]), 1),
                                        queue=queue, prefetched=pre))
+
+    def _issue_prefetch(self, l: int, step: int, box: Dict) -> None:
+        """Issue lists cut at the cache size (a prefetch never evicts one of a layer's C
+        most likely experts to make room for another) into the next layers' caches."""
+        try:
+            queue = self.spec.queue(self.m.C)
+            box["queue"] = queue
+            box["prefetched"] = [self.cache.prefetch(l + 1 + j, step, q, self.prefetch["max_prefetch"],
+                                                     copy_stream=self.copy_stream) for j, q in enumerate(queue)]
+        except BaseException as ex:  # re-raised on the calling thread
+            box["error"] = ex
+
+    def _rollout(self, future, x) -> None:
+        pf = self.prefetch
+        if self.spec_events is None:
+            self.spec.run(future, x, pf["l_min"], pf["tau"])
+            return
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        self.spec.run(future, x, pf["l_min"], pf["tau"])
+        e1.record()
+        self.spec_events.append((e0, e1, len(future)))
 
     def close(self) -> None:
         torch.cuda.synchronize()
