@@ -311,3 +311,33 @@ def prefetch_queue(n_experts: int, pred_idx, pred_prob, max_per_depth: int):
     ex = np.empty((D, max(max_per_depth, 1)), np.int32); cnt = np.empty(D, np.int32)
     lib().orc_prefetch_queue(n_experts, D, T, K, _ptr(pidx), _ptr(pprob), max_per_depth, _ptr(ex), _ptr(cnt))
     return [ex[i, :cnt[i]].tolist() for i in range(D)]
+
+
+# ---- LoRE calibration fit (Sec. 4.2, Eq. 8-10) ---------------------------------------------
+
+def lore_fit(X, Y, r: int):
+    """The minimiser of Eq. 10, sum_t || y_t - B A x_t ||^2 over A [r][d], B [d][r], in fp64.
+
+    X [n][d] calibration hidden states (rows), Y [n][d] their residual targets
+    E_e(x) - S(x) (Eq. 8).  This is reduced-rank regression: the least-squares map
+    W_ols = Y^T (X^T)^+ (minimum norm), its fitted values F = W_ols X^T, and the best rank-r
+    approximation of F from its r leading left singular vectors U_r (Eckart-Young), so
+    B A = U_r U_r^T W_ols with B = U_r, A = U_r^T W_ols.  Returns (A, B, loss)."""
+    X = np.asarray(X, np.float64)
+    Y = np.asarray(Y, np.float64)
+    Xt, Yt = X.T, Y.T  # columns are tokens
+    W_ols = Yt @ np.linalg.pinv(Xt)
+    F = W_ols @ Xt
+    U, _, _ = np.linalg.svd(F, full_matrices=False)
+    Ur = U[:, :r]
+    B = Ur
+    A = Ur.T @ W_ols
+    R = Yt - B @ (A @ Xt)
+    return A, B, float((R * R).sum())
+
+
+def lore_loss(X, Y, A, B) -> float:
+    """Eq. 10's objective for given factors."""
+    X = np.asarray(X, np.float64); Y = np.asarray(Y, np.float64)
+    R = Y.T - np.asarray(B, np.float64) @ (np.asarray(A, np.float64) @ X.T)
+    return float((R * R).sum())
