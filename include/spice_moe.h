@@ -439,6 +439,32 @@ spice_status_t moe_cache_prefetch(spice_cache_t* cache, int32_t layer, int32_t s
                                   spice_stream_t compute_stream, int32_t* n_admitted, int32_t* admitted,
                                   int32_t* evicted);
 
+/*
+ * LoRE calibration fit (Sec. 4.2, Eq. 8-10) of one expert from n calibration tokens:
+ * the factors A [r][d], B [d][r] minimising sum_t || E_e(x_t) - S(x_t) - B A x_t ||^2.
+ * With n <= d tokens of full rank every residual is reachable, so the minimiser is the
+ * truncated SVD of the residual matrix carried back through the tokens' pseudo-inverse
+ * (minimum-norm A); the loss is the sum of the squared singular values beyond the r-th,
+ * and r >= n fits exactly (directions beyond n are zero rows of A / columns of B).
+ * E_e and S run on the GPU (the grouped-FFN kernels), the n x n Gram matrices in fp64 on
+ * the GPU, their eigen-decomposition and solve in fp64 on the host.  The call is
+ * synchronous: it returns when A and B are written.
+ *   n            calibration tokens, 1 <= n <= min(d, 1024)
+ *   r            rank, 1 <= r <= d (the LoRE rank; it may differ from cfg->lore_rank)
+ *   x            device [n][d] (dtype) calibration hidden states, linearly independent
+ *   w13, w2      device weights of the expert: [2I][d], [d][I] (dtype)
+ *   w13_shared, w2_shared  device shared block (ignored when cfg->shared_inter is 0)
+ *   A_out, B_out device fp32 [r][d] and [d][r] out
+ *   y_out        nullable device fp32 [n][d] out: the residual targets E_e(x) - S(x)
+ *   loss_out     nullable host out: Eq. 10's minimum (fp64, from the residual spectrum)
+ *   ws, ws_bytes workspace of spice_lore_fit_workspace_bytes(cfg, n, r) bytes
+ * Returns UNSUPPORTED for n > min(d, 1024), INVALID for linearly dependent tokens.
+ */
+size_t spice_lore_fit_workspace_bytes(const spice_moe_cfg_t* cfg, int32_t n, int32_t r);
+spice_status_t moe_lore_fit(const spice_moe_cfg_t* cfg, int32_t n, int32_t r, const void* x, const void* w13,
+                            const void* w2, const void* w13_shared, const void* w2_shared, float* A_out, float* B_out,
+                            float* y_out, double* loss_out, void* ws, size_t ws_bytes, spice_stream_t stream);
+
 /* Text of a status code, and the last error message of the calling thread. */
 const char* spice_status_string(spice_status_t status);
 const char* spice_last_error(void);

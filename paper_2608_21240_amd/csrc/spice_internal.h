@@ -163,6 +163,13 @@ hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn_fetched(const FfnArgs& a, const FetchArgs& f, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_spec_update(const SpecArgs& a, hipStream_t s);
+
+// LoRE calibration fit (lore_fit.hip).
+hipError_t launch_fit_setup(int32_t n, int32_t* perm, int32_t* offsets, int32_t* resident, hipStream_t s);
+hipError_t launch_fit_residual(size_t count, float* y, const float* shared, hipStream_t s);
+hipError_t launch_fit_gram(int32_t n, int32_t d, int dtype, const void* M, double* G, hipStream_t s);
+hipError_t launch_fit_project(int32_t n, int32_t d, int32_t r, int dtype, const void* M, const double* C, float* out,
+                              bool b_layout, hipStream_t s);
 hipError_t launch_fill_u32(uint32_t* p, size_t words, uint32_t value, hipStream_t s);
 
 }  // namespace spice

@@ -31,6 +31,7 @@ EXPORTS = (
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
     "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
     "moe_spec_update", "moe_prefetch_h_min", "moe_prefetch_queue", "moe_cache_prefetch",
+    "spice_lore_fit_workspace_bytes", "moe_lore_fit",
     "spice_status_string", "spice_last_error",
 )
 
@@ -110,6 +111,9 @@ def lib() -> ctypes.CDLL:
                                         ctypes.c_double]),
             "moe_prefetch_queue": (_I, [C, _I, _I, _P, _P, _I, _P, _P]),
             "moe_cache_prefetch": (_I, [_P, _I, _I, _I, _P, _I, _P, _P, _P, _P, _P]),
+            "spice_lore_fit_workspace_bytes": (_Z, [C, _I, _I]),
+            "moe_lore_fit": (_I, [C, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.POINTER(ctypes.c_double), _P, _Z,
+                                  _P]),
             "spice_status_string": (ctypes.c_char_p, [_I]),
             "spice_last_error": (ctypes.c_char_p, []),
         }
@@ -357,3 +361,13 @@ def moe_prefetch_queue(cfg, pred_idx_host, pred_prob_host, max_per_depth: int):
         ctypes.byref(cfg), T, D, pidx.ctypes.data, pprob.ctypes.data, max_per_depth, ex.ctypes.data,
         cnt.ctypes.data))
     return [ex[i, :cnt[i]].tolist() for i in range(D)]
+
+
+def moe_lore_fit(cfg, n, r, x, w13, w2, w13s, w2s, A_out, B_out, y_out=None, ws=None, ws_bytes=0,
+                 stream=None) -> float:
+    """LoRE calibration fit of one expert (Eq. 10); returns the minimum loss."""
+    loss = ctypes.c_double(0.0)
+    _check("moe_lore_fit", lib().moe_lore_fit(
+        ctypes.byref(cfg), n, r, _p(x), _p(w13), _p(w2), _p(w13s), _p(w2s), _p(A_out), _p(B_out), _p(y_out),
+        ctypes.byref(loss), _p(ws), ws_bytes, _stream(stream)))
+    return loss.value

@@ -153,3 +153,26 @@ def test_spec_update_validates_on_the_host():
     assert call(h_out=D + 64) == spice.SPICE_ERR_INVALID  # overlaps h_in without being it
     assert call(ws=None) == spice.SPICE_ERR_INVALID
     assert call(T=0, depth=1) == spice.SPICE_OK
+
+
+def test_lore_fit_validates_on_the_host():
+    L = spice.lib()
+    c = cfg()
+    D = DUMMY
+    ws = spice.spice_workspace_bytes(c, 8) * 8
+
+    def call(n=8, r=4, x=D, w13=D, w2=D, ws_=D, ws_bytes=ws):
+        return L.moe_lore_fit(ctypes.byref(c), n, r, x, w13, w2, D, D, D, D, None, None, ws_, ws_bytes, None)
+
+    assert call(n=0) == spice.SPICE_ERR_INVALID
+    assert call(n=c.d + 1) in (spice.SPICE_ERR_UNSUPPORTED, spice.SPICE_ERR_INVALID)
+    assert call(n=1025) in (spice.SPICE_ERR_UNSUPPORTED, spice.SPICE_ERR_INVALID)
+    assert call(r=0) == spice.SPICE_ERR_INVALID
+    assert call(r=c.d + 1) == spice.SPICE_ERR_INVALID
+    assert call(x=None) == spice.SPICE_ERR_INVALID
+    assert call(w2=None) == spice.SPICE_ERR_INVALID
+    assert call(ws_=None) == spice.SPICE_ERR_INVALID
+    assert call(ws_bytes=16) == spice.SPICE_ERR_WORKSPACE
+    assert L.spice_lore_fit_workspace_bytes(ctypes.byref(c), 0, 4) == 0
+    assert L.spice_lore_fit_workspace_bytes(ctypes.byref(c), 2000, 4) == 0
+    assert L.spice_lore_fit_workspace_bytes(ctypes.byref(c), 512, 32) > 512 * 512 * 16
