@@ -63,10 +63,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="finish with a plain device copy of this many MiB (a known-size reference for counters)")
-    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill", "dsv2_stack"),
+    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill", "dsv2_stack", "lore_fit"),
                    help="dsv2_decode: the decode layer (default); qwen2_prefill: the 4096-token "
                         "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path; dsv2_stack: the 26-layer "
-                        "LRU-cached decode stack with and without speculative prefetching")
+                        "LRU-cached decode stack with and without speculative prefetching; lore_fit: "
+                        "LoRE calibration fits of DSV2-Lite experts (512 tokens, rank 32)")
     p.add_argument("--spec-depth", type=int, default=2, help="dsv2_stack: lookahead layers of the draft rollout")
     p.add_argument("--spec-tau", type=float, default=0.0, help="dsv2_stack: halting threshold of the rollout")
     p.add_argument("--max-prefetch", type=int, default=3, help="dsv2_stack: prefetched experts per layer and call")
@@ -128,6 +129,8 @@ def main():
         return prefill_main(args)
     if args.workload == "dsv2_stack":
         return stack_main(args)
+    if args.workload == "lore_fit":
+        return lore_fit_main(args)
     batches = [int(b) for b in args.batches.split(",")]
     wl = W.WORKLOADS["dsv2_decode_t32"]
     shape = wl.shape
@@ -395,6 +398,51 @@ def stack_main(args):
                      "frac": round(on["rollout_GBps"] / HBM_PEAK_GBS, 4), "traffic": None,
                      "bytes_per_depth": on["bytes_per_depth"], "avg_depth_us": round(on["rollout_us_per_depth"], 2)},
         "by_mode": res,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def lore_fit_main(args):
+    """LoRE calibration fits (Eq. 10) of DSV2-Lite-shaped experts from 512 calibration tokens
+    at rank 32, one expert per step (rotating over 8 experts).  A step is one whole fit:
+    E_e and S on the tokens (MFMA GEMM path), residual, the two fp64 Gram matrices, the host
+    eigen-decomposition and solve, and the factor products.  The GPU part is timed with
+    events around the whole call less the host's own share, which the call cannot expose;
+    the rocprofv3 kernel trace gives the per-kernel split."""
+    import torch
+
+    from paper_2608_21240_amd import layer as LY, spice, synth, workloads as W
+
+    s = W.DSV2
+    n, r, E = 512, 32, 8
+    wl = W.Workload("lore_fit", s, tokens=n, resident=0, skew=False)
+    dt = s.dtype
+    experts = [tuple(LY.to_tensor(a, dt, "cuda") for a in synth.gen_expert(wl, 0, e)) for e in range(E)]
+    w13s, w2s = (LY.to_tensor(a, dt, "cuda") for a in synth.gen_shared(wl, 0))
+    X = LY.to_tensor(synth.gen_x(wl, 0, 0, n), dt, "cuda")
+    cfg = spice.make_cfg(s, 1)
+    A = torch.empty((r, s.d), dtype=torch.float32, device="cuda")
+    B = torch.empty((s.d, r), dtype=torch.float32, device="cuda")
+    wsb = spice.lib().spice_lore_fit_workspace_bytes(spice.ctypes.byref(cfg), n, r)
+    ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+    for k in range(args.warmup):
+        spice.moe_lore_fit(cfg, n, r, X, *experts[k % E], w13s, w2s, A, B, None, ws, wsb)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    losses = []
+    for k in range(args.steps):
+        losses.append(spice.moe_lore_fit(cfg, n, r, X, *experts[k % E], w13s, w2s, A, B, None, ws, wsb))
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    line = {
+        "metric": "LoRE calibration fits per second (DSV2-Lite expert, 512 tokens, rank 32)",
+        "value": round(args.steps / wall, 3), "unit": "fits/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(1e3 * wall / args.steps, 2), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16 in, fp32/fp64 fit",
+        "data": "synthetic (seeded random-init DSV2-Lite expert and shared block, N(0,1) calibration tokens)",
+        "config": {"workload": "lore_fit_dsv2_n512_r32", "tokens": n, "rank": r, "hidden": s.d, "inter": s.inter,
+                   "shared_inter": s.shared_inter},
+        "mean_loss": float(np.mean(losses)),
     }
     print(json.dumps(line), flush=True)
 

@@ -7,8 +7,8 @@
 //   Y = U S V^T,  B = U_r = Y V_r S_r^-1,  A = S_r V_r^T (X^T X)^-1 X^T,
 //   loss = sum_{i > r} s_i^2.
 // Everything n-dimensional is done on the host in fp64 from the two n x n Gram matrices
-// X^T X and Y^T Y (computed on the GPU in fp64): Y^T Y = V S^2 V^T by cyclic Jacobi
-// rotations, (X^T X) Z = V_r S_r by Cholesky.  The GPU computes E_e(x) and S(x) with the
+// X^T X and Y^T Y (computed on the GPU in fp64): Y^T Y = V S^2 V^T by Jacobi rotations
+// (round-robin order), (X^T X) Z = V_r S_r by Cholesky.  The GPU computes E_e(x) and S(x) with the
 // grouped-FFN kernels (a one-expert bucket of all n tokens), the residual, the Gram
 // matrices and the final d x r products.
 #include <hip/hip_runtime_api.h>
@@ -68,47 +68,75 @@ FitLayout fit_layout(const spice_moe_cfg_t& c, int32_t n, int32_t r) {
     return L;
 }
 
-// Eigen-decomposition of the symmetric n x n matrix a (destroyed) by cyclic Jacobi
-// rotations: a = V diag(w) V^T, V column-major in v (v[i + n*k] = component i of vector k).
-void jacobi_eigen(int n, std::vector<double>& a, std::vector<double>& w, std::vector<double>& v) {
-    v.assign((size_t)n * n, 0.0);
-    for (int i = 0; i < n; ++i) v[(size_t)i * n + i] = 1.0;
-    auto A = [&](int i, int j) -> double& { return a[(size_t)i * n + j]; };
+// Eigen-decomposition of the symmetric n x n matrix a (row-major, destroyed) by Jacobi
+// rotations in round-robin order: each round rotates n/2 disjoint index pairs at once
+// (every index meets every other once per sweep), applying all row rotations and then all
+// column rotations row by row, so that every access runs along a row.
+// a = V diag(w) V^T with the eigenvectors as the rows of vt (vt[k*n + i] = component i of
+// vector k).
+void jacobi_eigen(int n, std::vector<double>& a, std::vector<double>& w, std::vector<double>& vt) {
+    vt.assign((size_t)n * n, 0.0);
+    for (int i = 0; i < n; ++i) vt[(size_t)i * n + i] = 1.0;
+    const int m = n + (n & 1);  // players of the tournament; index n is a bye when n is odd
+    std::vector<int> player(m);
+    for (int i = 0; i < m; ++i) player[i] = i;
+    struct Rot {
+        int p, q;
+        double c, s;
+    };
+    std::vector<Rot> rots;
+    rots.reserve(m / 2);
+    auto rotate_rows = [&](double* base) {
+        for (const Rot& r : rots) {
+            double* rp = base + (size_t)r.p * n;
+            double* rq = base + (size_t)r.q * n;
+            for (int k = 0; k < n; ++k) {
+                const double ap = rp[k], aq = rq[k];
+                rp[k] = r.c * ap - r.s * aq;
+                rq[k] = r.s * ap + r.c * aq;
+            }
+        }
+    };
     for (int sweep = 0; sweep < 60; ++sweep) {
         double off = 0.0, diag = 0.0;
         for (int i = 0; i < n; ++i) {
-            diag += A(i, i) * A(i, i);
-            for (int j = i + 1; j < n; ++j) off += A(i, j) * A(i, j);
+            diag += a[(size_t)i * n + i] * a[(size_t)i * n + i];
+            for (int j = i + 1; j < n; ++j) off += a[(size_t)i * n + j] * a[(size_t)i * n + j];
         }
-        if (off <= 1e-30 * diag || off == 0.0) break;
-        for (int p = 0; p < n - 1; ++p)
-            for (int q = p + 1; q < n; ++q) {
-                const double apq = A(p, q);
+        if (off == 0.0 || off <= 1e-30 * diag) break;
+        for (int round = 0; round < m - 1; ++round) {
+            rots.clear();
+            for (int i = 0; i < m / 2; ++i) {
+                int p = player[i], q = player[m - 1 - i];
+                if (p > q) std::swap(p, q);
+                if (q >= n) continue;
+                const double apq = a[(size_t)p * n + q];
                 if (apq == 0.0) continue;
-                // rotation angle that zeroes a[p][q]: tan(2 theta) = 2 a_pq / (a_qq - a_pp)
-                const double theta = (A(q, q) - A(p, p)) / (2.0 * apq);
+                // the angle that zeroes a[p][q]: tan(2 theta) = 2 a_pq / (a_qq - a_pp)
+                const double theta = (a[(size_t)q * n + q] - a[(size_t)p * n + p]) / (2.0 * apq);
                 const double t = (theta >= 0 ? 1.0 : -1.0) / (std::fabs(theta) + std::sqrt(theta * theta + 1.0));
-                const double c = 1.0 / std::sqrt(t * t + 1.0), s = t * c;
-                for (int k = 0; k < n; ++k) {  // columns p and q
-                    const double akp = A(k, p), akq = A(k, q);
-                    A(k, p) = c * akp - s * akq;
-                    A(k, q) = s * akp + c * akq;
-                }
-                for (int k = 0; k < n; ++k) {  // rows p and q
-                    const double apk = A(p, k), aqk = A(q, k);
-                    A(p, k) = c * apk - s * aqk;
-                    A(q, k) = s * apk + c * aqk;
-                }
-                for (int k = 0; k < n; ++k) {
-                    double* vk = &v[(size_t)k];
-                    const double vp = vk[(size_t)n * p], vq = vk[(size_t)n * q];
-                    vk[(size_t)n * p] = c * vp - s * vq;
-                    vk[(size_t)n * q] = s * vp + c * vq;
+                const double c = 1.0 / std::sqrt(t * t + 1.0);
+                rots.push_back({p, q, c, t * c});
+            }
+            rotate_rows(a.data());
+            for (int k = 0; k < n; ++k) {  // the same rotations on the columns, row by row
+                double* row = a.data() + (size_t)k * n;
+                for (const Rot& r : rots) {
+                    const double ap = row[r.p], aq = row[r.q];
+                    row[r.p] = r.c * ap - r.s * aq;
+                    row[r.q] = r.s * ap + r.c * aq;
                 }
             }
+            for (const Rot& r : rots) a[(size_t)r.p * n + r.q] = a[(size_t)r.q * n + r.p] = 0.0;
+            rotate_rows(vt.data());
+            // next round: the first player stays, the others move one place round the circle
+            const int last = player[m - 1];
+            for (int i = m - 1; i > 1; --i) player[i] = player[i - 1];
+            player[1] = last;
+        }
     }
     w.resize(n);
-    for (int i = 0; i < n; ++i) w[i] = A(i, i);
+    for (int i = 0; i < n; ++i) w[i] = a[(size_t)i * n + i];
 }
 
 // Cholesky factor of the SPD n x n matrix g (row-major, lower factor in place); false if

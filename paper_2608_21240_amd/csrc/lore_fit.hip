@@ -70,26 +70,17 @@ __global__ __launch_bounds__(kGramThreads) void fit_gram_kernel(int32_t n, int32
     }
 }
 
-// out[k][j] (b_layout) or out[j][k] = sum_i M[i][k] C[i][j] for feature k = one thread,
-// j < r in chunks of 16 accumulators.
+// out[k][j] (b_layout) or out[j][k] = sum_i M[i][k] C[i][j]: one thread per (feature k,
+// column j); a block takes 256 consecutive features of one column, so the rows of M are
+// read coalesced and C[i][j] is the same for the whole block.
 __global__ __launch_bounds__(256) void fit_project_kernel(int32_t n, int32_t d, int32_t r, int dtype, const void* M,
                                                           const double* C, float* out, int b_layout) {
-    const int k = blockIdx.x * blockDim.x + threadIdx.x;
+    const int k = blockIdx.x * blockDim.x + threadIdx.x, j = blockIdx.y;
     if (k >= d) return;
-    for (int j0 = 0; j0 < r; j0 += 16) {
-        double acc[16];
-        for (int j = 0; j < 16; ++j) acc[j] = 0.0;
-        for (int i = 0; i < n; ++i) {
-            const double m = elem(M, dtype, (size_t)i * d + k);
-            const double* c = C + (size_t)i * r + j0;
-            for (int j = 0; j < 16; ++j)
-                if (j0 + j < r) acc[j] += m * c[j];
-        }
-        for (int j = 0; j < 16 && j0 + j < r; ++j) {
-            if (b_layout) out[(size_t)k * r + j0 + j] = (float)acc[j];
-            else out[(size_t)(j0 + j) * d + k] = (float)acc[j];
-        }
-    }
+    double acc = 0.0;
+    for (int i = 0; i < n; ++i) acc += elem(M, dtype, (size_t)i * d + k) * C[(size_t)i * r + j];
+    if (b_layout) out[(size_t)k * r + j] = (float)acc;
+    else out[(size_t)j * d + k] = (float)acc;
 }
 
 }  // namespace
@@ -115,8 +106,8 @@ hipError_t launch_fit_gram(int32_t n, int32_t d, int dtype, const void* M, doubl
 
 hipError_t launch_fit_project(int32_t n, int32_t d, int32_t r, int dtype, const void* M, const double* C, float* out,
                               bool b_layout, hipStream_t s) {
-    hipLaunchKernelGGL(fit_project_kernel, dim3((unsigned)((d + 255) / 256)), dim3(256), 0, s, n, d, r, dtype, M, C,
-                       out, b_layout ? 1 : 0);
+    hipLaunchKernelGGL(fit_project_kernel, dim3((unsigned)((d + 255) / 256), (unsigned)r), dim3(256), 0, s, n, d, r,
+                       dtype, M, C, out, b_layout ? 1 : 0);
     return hipGetLastError();
 }
 
