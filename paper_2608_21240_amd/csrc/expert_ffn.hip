@@ -5,9 +5,9 @@
 //   up   : 16-row tiles of W1/W3 (or of A_e): H = silu(X W1^T) * (X W3^T)  (or U = X A_e^T),
 //          X = the tokens of the expert's bucket;
 //   down : 32-row tiles of W2: Y = H W2^T;  256-row tiles of B_e: delta = U B_e^T.
-// Blocks map to (expert ordinal, row tile): HIT experts first, then the shared
-// block, then LORE experts.  Each wave resolves its block's expert on the device
-// from the bucket offsets (the pool slot comes in the same round trip), so no
+// Blocks map to (expert ordinal, row tile): the shared block first, then LORE
+// experts, then HIT experts (longest tiles first).  Each wave resolves its block's
+// expert on the device from the bucket offsets (the pool slot comes in the same round trip), so no
 // host synchronisation is needed and blocks beyond the live experts exit at once;
 // the hardware dispatcher overlaps one block's set-up with the others' streaming.
 // Within a tile the 4 waves split the contraction dimension and add their MFMA

@@ -120,32 +120,25 @@ __device__ bool find_group(const FfnArgs& a, int c, int j, Group& g) {
     return false;
 }
 
-// Token of bucket position pos (0, flagged, if perm holds garbage).
-__device__ __forceinline__ int token_of(const FfnArgs& a, int pos) {
-    const int s = a.perm[pos];
-    if (s < 0 || s >= a.T * a.K) {
-        atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
-        return 0;
-    }
-    return s / a.K;
-}
-
 enum : int { kKindHit = 0, kKindShared = 1, kKindLore = 2 };
 
 struct Tile {
     int kind, ordinal, rt;
 };
 
-// Block index -> tile.  Segments: HIT experts x row tiles, shared-block row tiles,
-// LORE experts x row tiles (expert counts are upper bounds; surplus blocks exit).
+// Block index -> tile.  Segments, in dispatch order: shared-block row tiles (the
+// longest tiles: all T tokens, and the longest contraction in the down pass), LORE
+// experts x row tiles (short but latency-bound), HIT experts x row tiles.  Putting
+// the long tiles first keeps them out of the launch's tail.  Expert counts are upper
+// bounds; surplus blocks exit at once.
 struct Grid {
     int nhit, thit, tsh, nlore, tlore;
     __device__ bool decode(int b, Tile& t) const {
-        if (b < nhit * thit) { t = {kKindHit, b / thit, b % thit}; return true; }
-        b -= nhit * thit;
         if (b < tsh) { t = {kKindShared, 0, b}; return true; }
         b -= tsh;
         if (b < nlore * tlore) { t = {kKindLore, b / tlore, b % tlore}; return true; }
+        b -= nlore * tlore;
+        if (b < nhit * thit) { t = {kKindHit, b / thit, b % thit}; return true; }
         return false;
     }
 };
@@ -154,56 +147,102 @@ struct Grid {
 // MFMA main loop shared by both launches.
 //   a[i]: per-lane pointer to weight row (tile row m = lane & 15) at the lane's k offset
 //   b[j]: per-lane pointer to the token row (column m) at the lane's k offset
-// Contraction steps [ks0, ks1) are all full (every lane's 16-byte chunk in range).
-// Loads of U steps are issued before their MFMAs so that many bytes are in flight.
+// The contraction is cut into whole groups of U full steps, dealt to the 4 waves; the
+// last wave also does the steps left over.  The wave index is read as a uniform value,
+// so the loop bounds live in scalar registers and the group loop has no divergent
+// branches: its loads are unconditional and in order, and the wait before each MFMA
+// leaves the next group's loads in flight (two groups per wave).
 // ---------------------------------------------------------------------------
 constexpr int kStepBytes = 64;  // 32 bf16 or 16 fp32 per step per 4 lanes; same byte stride
 
+// Steps per load group: 4 with three operand streams (two weight tiles and one token tile,
+// or one and two), 2 with four; two groups are in flight, which fits 3 waves per SIMD.
+#define SPICE_GROUP_STEPS(NA, NB) (((NA) + (NB) <= 3) ? 4 : 2)
+
+// Loads of the U steps [sg, sg + U) of one group: unconditional, at immediate offsets
+// from one address per operand stream.
 template <int DT, int NA, int NB>
-__device__ __forceinline__ void mma_steps(const char* const (&a)[NA], const char* const (&b)[NB], int ks0, int ks1,
-                                          f32x4_t (&acc)[NA][NB]) {
-    constexpr int U = (NA + NB <= 3) ? 8 : 4;
-    using T_ = Tr<DT>;
-    int ks = ks0;
-    for (; ks + U <= ks1; ks += U) {
-        u32x4_t av[NA][U], bv[NB][U];
-        const size_t off = (size_t)ks * kStepBytes;
+__device__ __forceinline__ void mma_load(const char* const (&a)[NA], const char* const (&b)[NB], int sg,
+                                         u32x4_t (&av)[NA][SPICE_GROUP_STEPS(NA, NB)],
+                                         u32x4_t (&bv)[NB][SPICE_GROUP_STEPS(NA, NB)]) {
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
+    const size_t off = (size_t)sg * kStepBytes;
+    // weight loads first: they depend only on the expert's pool slot, while the token
+    // rows wait for the bucket's token ids
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
+    for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int i = 0; i < NA; ++i) av[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off + u * kStepBytes);
+        for (int i = 0; i < NA; ++i) av[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off + u * kStepBytes);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-            for (int j = 0; j < NB; ++j) bv[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off + u * kStepBytes);
-        }
-        __builtin_amdgcn_sched_barrier(0);  // keep every load of the group ahead of its MFMAs
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < NB; ++j) bv[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off + u * kStepBytes);
+}
+
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_comp(const u32x4_t (&av)[NA][SPICE_GROUP_STEPS(NA, NB)],
+                                         const u32x4_t (&bv)[NB][SPICE_GROUP_STEPS(NA, NB)],
+                                         f32x4_t (&acc)[NA][NB]) {
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int i = 0; i < NA; ++i) acc[i][j] = Tr<DT>::mma(av[i][u], bv[j][u], acc[i][j]);
+}
+
+// ng whole groups starting at step s0 (uniform), two groups in flight: the loads of
+// group g+1 go out before the MFMAs of group g.  The steady-state body loads
+// unconditionally, so the wait before each MFMA leaves the next group's loads pending.
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_groups(const char* const (&a)[NA], const char* const (&b)[NB], int s0, int ng,
+                                           f32x4_t (&acc)[NA][NB], u32x4_t (&a0)[NA][SPICE_GROUP_STEPS(NA, NB)]) {
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
+    if (ng <= 0) return;
+    u32x4_t b0[NB][U], a1[NA][U], b1[NB][U];
+    {  // a0 already holds the weights of group 0 (mma_first_a); its token rows now
+        const size_t off = (size_t)s0 * kStepBytes;
 #pragma unroll
         for (int u = 0; u < U; ++u)
 #pragma unroll
-            for (int j = 0; j < NB; ++j)
-#pragma unroll
-                for (int i = 0; i < NA; ++i) acc[i][j] = T_::mma(av[i][u], bv[j][u], acc[i][j]);
+            for (int j = 0; j < NB; ++j) b0[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off + u * kStepBytes);
     }
-    const int rem = ks1 - ks;  // 0 .. U-1 steps left: one more group, loads clamped to the last step
-    if (rem > 0) {
-        u32x4_t av[NA][U], bv[NB][U];
-#pragma unroll
-        for (int u = 0; u < U; ++u) {
-            const size_t off = (size_t)(ks + min(u, rem - 1)) * kStepBytes;
-#pragma unroll
-            for (int i = 0; i < NA; ++i) av[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off);
-#pragma unroll
-            for (int j = 0; j < NB; ++j) bv[j][u] = *reinterpret_cast<const u32x4_t*>(b[j] + off);
-        }
+    int g = 0;
+    for (; g + 2 < ng; g += 2) {
+        mma_load<DT, NA, NB>(a, b, s0 + (g + 1) * U, a1, b1);
         __builtin_amdgcn_sched_barrier(0);
+        mma_comp<DT, NA, NB>(a0, b0, acc);
+        mma_load<DT, NA, NB>(a, b, s0 + (g + 2) * U, a0, b0);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_comp<DT, NA, NB>(a1, b1, acc);
+    }
+    if (g + 1 < ng) {
+        mma_load<DT, NA, NB>(a, b, s0 + (g + 1) * U, a1, b1);
+        __builtin_amdgcn_sched_barrier(0);
+        mma_comp<DT, NA, NB>(a0, b0, acc);
+        mma_comp<DT, NA, NB>(a1, b1, acc);
+    } else {
+        mma_comp<DT, NA, NB>(a0, b0, acc);
+    }
+}
+
+// Single full steps [ks0, ks1) (the few left over after the whole groups).
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_singles(const char* const (&a)[NA], const char* const (&b)[NB], int ks0, int ks1,
+                                            f32x4_t (&acc)[NA][NB]) {
+    for (int ks = ks0; ks < ks1; ++ks) {
+        const size_t off = (size_t)ks * kStepBytes;
+        u32x4_t av[NA], bv[NB];
 #pragma unroll
-        for (int u = 0; u < U; ++u) {
-            if (u < rem) {  // uniform across the wave
+        for (int i = 0; i < NA; ++i) av[i] = *reinterpret_cast<const u32x4_t*>(a[i] + off);
 #pragma unroll
-                for (int j = 0; j < NB; ++j)
+        for (int j = 0; j < NB; ++j) bv[j] = *reinterpret_cast<const u32x4_t*>(b[j] + off);
 #pragma unroll
-                    for (int i = 0; i < NA; ++i) acc[i][j] = T_::mma(av[i][u], bv[j][u], acc[i][j]);
-            }
-        }
+        for (int j = 0; j < NB; ++j)
+#pragma unroll
+            for (int i = 0; i < NA; ++i) acc[i][j] = Tr<DT>::mma(av[i], bv[j], acc[i][j]);
     }
 }
 
@@ -225,41 +264,98 @@ __device__ __forceinline__ void mma_tail(const char* const (&a)[NA], const char*
         for (int i = 0; i < NA; ++i) acc[i][j] = Tr<DT>::mma(av[i], bv[j], acc[i][j]);
 }
 
-// One wave's share of a (NA row streams) x (NB token tiles) product over kdim.
+// The whole groups of U full steps of kdim are dealt to the waves (w uniform); the
+// last wave also takes the full steps left over and the partial step, if any.
+template <int DT, int NA, int NB>
+struct WaveGroups {
+    int g0, g1;
+    __device__ WaveGroups(int kdim, int w) {
+        const int ngr = (kdim / Tr<DT>::kStep) / SPICE_GROUP_STEPS(NA, NB);
+        g0 = w * ngr / kWaves;
+        g1 = (w + 1) * ngr / kWaves;
+    }
+};
+
+// Weight loads of this wave's first group, issued before the token rows are known.
+template <int DT, int NA, int NB>
+__device__ __forceinline__ void mma_first_a(const char* const (&a)[NA], int kdim, int w,
+                                            u32x4_t (&a0)[NA][SPICE_GROUP_STEPS(NA, NB)]) {
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
+    const WaveGroups<DT, NA, NB> wg(kdim, w);
+    if (wg.g1 > wg.g0) {
+        const size_t off = (size_t)wg.g0 * U * kStepBytes;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int i = 0; i < NA; ++i) a0[i][u] = *reinterpret_cast<const u32x4_t*>(a[i] + off + u * kStepBytes);
+    }
+}
+
+// One wave's share of a (NA row streams) x (NB token tiles) product over kdim; a0 holds
+// the weights of the wave's first group (mma_first_a).
 template <int DT, int NA, int NB>
 __device__ __forceinline__ void wave_product(const char* const (&a)[NA], const char* const (&b)[NB], int kdim, int w,
-                                             int quad, f32x4_t (&acc)[NA][NB]) {
+                                             int quad, f32x4_t (&acc)[NA][NB],
+                                             u32x4_t (&a0)[NA][SPICE_GROUP_STEPS(NA, NB)]) {
     constexpr int kStep = Tr<DT>::kStep;
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
 #pragma unroll
     for (int i = 0; i < NA; ++i)
 #pragma unroll
         for (int j = 0; j < NB; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    const int nfull = kdim / kStep;
-    const int nks = (kdim + kStep - 1) / kStep;
-    const int ks0 = w * nks / kWaves, ks1 = (w + 1) * nks / kWaves;
-    mma_steps<DT, NA, NB>(a, b, ks0, min(ks1, nfull), acc);
-    if (ks1 > nfull && nfull >= ks0)  // this wave owns the partial step
-        mma_tail<DT, NA, NB>(a, b, nfull, nfull * kStep + quad * Tr<DT>::kLaneK < kdim, acc);
+    const WaveGroups<DT, NA, NB> wg(kdim, w);
+    mma_groups<DT, NA, NB>(a, b, wg.g0 * U, wg.g1 - wg.g0, acc, a0);
+    if (w == kWaves - 1) {
+        const int nfull = kdim / kStep;
+        mma_singles<DT, NA, NB>(a, b, (nfull / U) * U, nfull, acc);
+        if (nfull * kStep < kdim)  // the partial step
+            mma_tail<DT, NA, NB>(a, b, nfull, nfull * kStep + quad * Tr<DT>::kLaneK < kdim, acc);
+    }
 }
 
 // ---------------------------------------------------------------------------
 // up: gate/up SwiGLU rows (HIT, shared) or A_e rows (LORE)
 // ---------------------------------------------------------------------------
+// Token ids of bucket positions p0 and p1 (p1 only with two token tiles): both loads go
+// out before either is checked.  Garbage in perm gives token 0 and a flag.
+template <int NB>
+__device__ __forceinline__ void token_ids(const FfnArgs& a, int p0, int p1, int& t0, int& t1) {
+    const int s0 = a.perm[p0];
+    const int s1 = (NB == 2) ? a.perm[p1] : 0;
+    __builtin_amdgcn_sched_barrier(0);  // both loads out before the first wait
+    const int TK = a.T * a.K;
+    const bool bad0 = s0 < 0 || s0 >= TK, bad1 = (NB == 2) && (s1 < 0 || s1 >= TK);
+    if (bad0 || bad1) atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+    t0 = bad0 ? 0 : s0 / a.K;
+    t1 = (NB == 2 && !bad1) ? s1 / a.K : 0;
+}
+
+// One token group of an up tile: the weight loads of the first group go out, then the
+// token ids are read (bucket tiles) and the product runs.
 template <int DT, int NB, bool kUp>
-__device__ __forceinline__ void up_pass(const char* gate, const char* up, const char* const (&xb)[NB], int kdim, int w,
-                                        int quad, f32x4_t (&red)[kWaves][kTokTiles][2][64], int lane) {
-    if constexpr (kUp) {
-        const char* const a[2] = {gate, up};
-        f32x4_t acc[2][NB];
-        wave_product<DT, 2, NB>(a, xb, kdim, w, quad, acc);
+__device__ __forceinline__ void up_pass(const FfnArgs& a, const char* gate, const char* up, bool bucket, int start,
+                                        int gi0, int gi1, size_t kb, int w, int quad,
+                                        f32x4_t (&red)[kWaves][kTokTiles][2][64], int lane) {
+    constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
+    constexpr int NA = kUp ? 2 : 1;
+    constexpr int U = SPICE_GROUP_STEPS(NA, NB);
+    const char* p[NA];
+    p[0] = gate;
+    if constexpr (NA == 2) p[1] = up;
+    u32x4_t a0[NA][U];
+    mma_first_a<DT, NA, NB>(p, a.d, w, a0);
+    __builtin_amdgcn_sched_barrier(0);
+    int t0 = gi0, t1 = gi1;
+    if (bucket) token_ids<NB>(a, start + gi0, start + gi1, t0, t1);
+    const char* xn[NB];
+    xn[0] = static_cast<const char*>(a.x) + (size_t)t0 * a.d * es + kb;
+    if constexpr (NB == 2) xn[1] = static_cast<const char*>(a.x) + (size_t)t1 * a.d * es + kb;
+    f32x4_t acc[NA][NB];
+    wave_product<DT, NA, NB>(p, xn, a.d, w, quad, acc, a0);
 #pragma unroll
-        for (int j = 0; j < NB; ++j) { red[w][j][0][lane] = acc[0][j]; red[w][j][1][lane] = acc[1][j]; }
-    } else {
-        const char* const a[1] = {gate};
-        f32x4_t acc[1][NB];
-        wave_product<DT, 1, NB>(a, xb, kdim, w, quad, acc);
-#pragma unroll
-        for (int j = 0; j < NB; ++j) red[w][j][0][lane] = acc[0][j];
+    for (int j = 0; j < NB; ++j) {
+        red[w][j][0][lane] = acc[0][j];
+        if constexpr (kUp) red[w][j][1][lane] = acc[NA - 1][j];
     }
 }
 
@@ -267,7 +363,8 @@ template <int DT>
 __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x4_t (&red)[kWaves][kTokTiles][2][64]) {
     using T_ = Tr<DT>;
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
     const void* wbase;
     size_t gate_row0, up_row0;
     int nrows, start = 0, n = a.T;
@@ -303,17 +400,13 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
         // padding columns read the bucket's last token; their outputs are dropped
         const int gi0 = min(g0 + m, n - 1), gi1 = min(g0 + 16 + m, n - 1);
-        const int t0 = (tile.kind == kKindShared) ? gi0 : token_of(a, start + gi0);
-        const int t1 = (tile.kind == kKindShared) ? gi1 : token_of(a, start + gi1);
-        const char* const xb[kTokTiles] = {static_cast<const char*>(a.x) + (size_t)t0 * a.d * es + kb,
-                                           static_cast<const char*>(a.x) + (size_t)t1 * a.d * es + kb};
-        const char* const x1[1] = {xb[0]};
+        const bool bucket = tile.kind != kKindShared;  // shared tiles take tokens 0..T-1 in order
         if (tile.kind == kKindLore) {
-            if (ntt == 1) up_pass<DT, 1, false>(gate, up, x1, a.d, w, quad, red, lane);
-            else up_pass<DT, 2, false>(gate, up, xb, a.d, w, quad, red, lane);
+            if (ntt == 1) up_pass<DT, 1, false>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
+            else up_pass<DT, 2, false>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
         } else {
-            if (ntt == 1) up_pass<DT, 1, true>(gate, up, x1, a.d, w, quad, red, lane);
-            else up_pass<DT, 2, true>(gate, up, xb, a.d, w, quad, red, lane);
+            if (ntt == 1) up_pass<DT, 1, true>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
+            else up_pass<DT, 2, true>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
         }
         __syncthreads();
         if (w < ntt) {
@@ -350,58 +443,82 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
 // ---------------------------------------------------------------------------
 // down: W2 rows (HIT, shared) with the MFMA path, B_e rows (LORE) on vector ALUs
 // ---------------------------------------------------------------------------
+// B_e rows of a LoRE tile, one row per thread, on vector ALUs (the rank is too small for
+// MFMA): delta[t][row] = sum_q B[row][q] U[t][q].  Each pass over kLoreChunk ranks issues
+// the row's B loads first, then stages U for up to kLoreTok tokens in LDS.
 template <int DT>
 __device__ void lore_down_tile(const FfnArgs& a, int expert, int start, int n, int rt, float* s_u) {
+    constexpr int L = Tr<DT>::kLaneK;  // elements per 16-byte load
+    constexpr int kLoreChunk = 64;
+    constexpr int NL = kLoreChunk / L;
+    constexpr int kUPer = kLoreTok * kLoreChunk / kThreads;  // U values staged per thread
     const int tid = threadIdx.x;
     const int row = rt * kLoreRows + tid;
     const bool row_ok = row < a.d;
     const size_t brow = ((size_t)expert * a.d + (row_ok ? row : 0)) * (size_t)a.r;
+    const u32x4_t zero = {0u, 0u, 0u, 0u};
     for (int g0 = 0; g0 < n; g0 += kLoreTok) {
         const int nt = min(kLoreTok, n - g0);
-        for (int i = tid; i < nt * a.r; i += kThreads) {
-            const int j = i / a.r, q = i - j * a.r;
-            s_u[j * a.r + q] = a.u[(size_t)(start + g0 + j) * a.r + q];
-        }
-        __syncthreads();
         float acc[kLoreTok];
 #pragma unroll
         for (int j = 0; j < kLoreTok; ++j) acc[j] = 0.f;
-        if (row_ok) {
-            for (int q = 0; q < a.r; q += Tr<DT>::kLaneK) {
-                const u32x4_t raw = Tr<DT>::load(a.lore_B, brow + q);
-                float bv[8];
-                if (DT == SPICE_BF16) {
-                    const uint32_t wv[4] = {raw.x, raw.y, raw.z, raw.w};
+        for (int q0 = 0; q0 < a.r; q0 += kLoreChunk) {
+            const int nq = min(kLoreChunk, a.r - q0);
+            u32x4_t raw[NL];
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) {
-                        bv[2 * i] = __uint_as_float(wv[i] << 16);
-                        bv[2 * i + 1] = __uint_as_float(wv[i] & 0xFFFF0000u);
-                    }
-                } else {
-                    bv[0] = __uint_as_float(raw.x); bv[1] = __uint_as_float(raw.y);
-                    bv[2] = __uint_as_float(raw.z); bv[3] = __uint_as_float(raw.w);
-                }
+            for (int i = 0; i < NL; ++i) raw[i] = (i * L < nq) ? Tr<DT>::load(a.lore_B, brow + q0 + i * L) : zero;
+            float uv[kUPer];
 #pragma unroll
-                for (int j = 0; j < kLoreTok; ++j) {
-                    if (j < nt) {
+            for (int i = 0; i < kUPer; ++i) {
+                const int idx = tid + i * kThreads, j = idx / kLoreChunk, q = idx - j * kLoreChunk;
+                uv[i] = (j < nt && q < nq) ? a.u[(size_t)(start + g0 + j) * a.r + q0 + q] : 0.f;
+            }
 #pragma unroll
-                        for (int qq = 0; qq < Tr<DT>::kLaneK; ++qq) acc[j] += bv[qq] * s_u[j * a.r + q + qq];
+            for (int i = 0; i < kUPer; ++i) s_u[tid + i * kThreads] = uv[i];
+            __syncthreads();
+            if (row_ok) {
+#pragma unroll
+                for (int i = 0; i < NL; ++i) {
+                    if (i * L < nq) {
+                        float bv[L];
+                        if constexpr (DT == SPICE_BF16) {
+                            const uint32_t wv[4] = {raw[i].x, raw[i].y, raw[i].z, raw[i].w};
+#pragma unroll
+                            for (int k = 0; k < 4; ++k) {
+                                bv[2 * k] = __uint_as_float(wv[k] << 16);
+                                bv[2 * k + 1] = __uint_as_float(wv[k] & 0xFFFF0000u);
+                            }
+                        } else {
+                            bv[0] = __uint_as_float(raw[i].x); bv[1] = __uint_as_float(raw[i].y);
+                            bv[2] = __uint_as_float(raw[i].z); bv[3] = __uint_as_float(raw[i].w);
+                        }
+#pragma unroll
+                        for (int j = 0; j < kLoreTok; ++j) {
+                            if (j < nt) {
+#pragma unroll
+                                for (int qq = 0; qq < L; ++qq) acc[j] += bv[qq] * s_u[j * kLoreChunk + i * L + qq];
+                            }
+                        }
                     }
                 }
             }
+            __syncthreads();
+        }
+        if (row_ok) {
 #pragma unroll
             for (int j = 0; j < kLoreTok; ++j)
                 if (j < nt) a.y_slots[(size_t)(start + g0 + j) * a.d + row] = acc[j];
         }
-        __syncthreads();
     }
 }
 
 template <int DT, int NA, int NB>
 __device__ __forceinline__ void down_pass(const char* const (&a)[NA], const char* const (&hb)[NB], int kdim,
                                           int w, int quad, f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64], int lane) {
+    u32x4_t a0[NA][SPICE_GROUP_STEPS(NA, NB)];
+    mma_first_a<DT, NA, NB>(a, kdim, w, a0);
     f32x4_t acc[NA][NB];
-    wave_product<DT, NA, NB>(a, hb, kdim, w, quad, acc);
+    wave_product<DT, NA, NB>(a, hb, kdim, w, quad, acc, a0);
 #pragma unroll
     for (int rr = 0; rr < NA; ++rr)
 #pragma unroll
@@ -413,7 +530,8 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
                           f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64]) {
     using T_ = Tr<DT>;
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
-    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
     const void* wbase;
     const void* hbase;
     int kdim, start = 0, n = a.T;
