@@ -76,6 +76,10 @@ def _declare(L: ctypes.CDLL) -> None:
     L.orc_lore_delta.argtypes = [_I, _I, _I, _P, _P, _P, _P]
     L.orc_token_output.argtypes = [cp, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
     L.orc_token_output.restype = _I
+    L.orc_token_output_sg.argtypes = [cp, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P]
+    L.orc_token_output_sg.restype = _I
+    L.orc_shared_gate.argtypes = [_I, _I, _P, _P]
+    L.orc_shared_gate.restype = ctypes.c_double
     L.orc_exact_residual.argtypes = [cp, _I, _P, _P, _P, _P, _P, _P, _P]
     L.orc_exact_residual.restype = _I
     L.orc_lru_step.argtypes = [_I, _I, _P, _P, _I, _I, _I, _P, _P, _I, _P, _P]
@@ -170,16 +174,25 @@ def lore_delta(d: int, r: int, dtype: int, A, B, x64):
     return y
 
 
-def token_output(cfg: Cfg, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, lA, lB):
-    """Per-token layer output.  w13/w2/lA/lB: length-N sequences (None where unused)."""
+def shared_gate(cfg: Cfg, x_row, w_sg) -> float:
+    """The shared block's output gate sigmoid(w_sg . x) for one token."""
+    x_row = _store(x_row, cfg.dtype); w = _store(w_sg, cfg.dtype)
+    return lib().orc_shared_gate(cfg.d, cfg.dtype, _ptr(x_row), _ptr(w))
+
+
+def token_output(cfg: Cfg, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, lA, lB, w_sg=None):
+    """Per-token layer output.  w13/w2/lA/lB: length-N sequences (None where unused);
+    w_sg: the shared block's gate vector [d], or None for an ungated shared block."""
     x_row = _store(x_row, cfg.dtype)
     idx_t = _c(idx_t, np.int32); g_t = _c(g_t, np.float64); cls_t = _c(cls_t, np.uint8)
     t13, k1 = _table(w13, cfg.dtype); t2, k2 = _table(w2, cfg.dtype)
     tA, k3 = _table(lA, cfg.dtype); tB, k4 = _table(lB, cfg.dtype)
     s13, s2 = _store(w13s, cfg.dtype), _store(w2s, cfg.dtype)
+    sg = None if w_sg is None else _store(w_sg, cfg.dtype)
     out = np.empty(cfg.d); ys = np.empty(cfg.d); yslot = np.empty((cfg.top_k, cfg.d))
-    rc = lib().orc_token_output(ctypes.byref(cfg), _ptr(x_row), _ptr(idx_t), _ptr(g_t), _ptr(cls_t),
-                                t13, t2, _ptr(s13), _ptr(s2), tA, tB, _ptr(out), _ptr(ys), _ptr(yslot))
+    rc = lib().orc_token_output_sg(ctypes.byref(cfg), _ptr(x_row), _ptr(idx_t), _ptr(g_t), _ptr(cls_t),
+                                   t13, t2, _ptr(s13), _ptr(s2), _ptr(sg), tA, tB, _ptr(out), _ptr(ys),
+                                   _ptr(yslot))
     if rc != 0:
         raise ValueError("oracle: a needed expert weight was not supplied")
     return out, ys, yslot
@@ -240,8 +253,9 @@ def route(cfg: Cfg, x, wg, bias, resident_mask, conf_in=None) -> Dict[str, np.nd
 
 
 def layer(cfg: Cfg, x, wg, bias, resident_mask, conf_in, w13, w2, w13s, w2s, lA, lB,
-          tokens: Optional[Sequence[int]] = None) -> Dict[str, np.ndarray]:
-    """Whole layer: routing for all tokens, outputs for ``tokens`` (default: all)."""
+          tokens: Optional[Sequence[int]] = None, w_sg=None) -> Dict[str, np.ndarray]:
+    """Whole layer: routing for all tokens, outputs for ``tokens`` (default: all); w_sg
+    gates the shared block (None: ungated)."""
     r = route(cfg, x, wg, bias, resident_mask, conf_in)
     T = x.shape[0]
     toks = list(range(T)) if tokens is None else list(tokens)
@@ -249,7 +263,7 @@ def layer(cfg: Cfg, x, wg, bias, resident_mask, conf_in, w13, w2, w13s, w2s, lA,
     yslot = np.empty((len(toks), cfg.top_k, cfg.d))
     for i, t in enumerate(toks):
         out[i], ys[i], yslot[i] = token_output(cfg, x[t], r["idx"][t], r["g"][t], r["cls"][t],
-                                               w13, w2, w13s, w2s, lA, lB)
+                                               w13, w2, w13s, w2s, lA, lB, w_sg)
     r.update(out=out, y_shared=ys, y_slot=yslot, tokens=np.array(toks, np.int32))
     return r
 

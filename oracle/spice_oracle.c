@@ -195,12 +195,29 @@ void orc_lore_delta(int32_t d, int32_t r, int32_t dtype, const void* A, const vo
     free(u);
 }
 
+/* Gated shared block: S(x) = sigmoid(w_sg . x) SwiGLU_s(x), the shared expert with its
+ * output gate (the Qwen2-style shared expert; the paper calls S the native shared expert). */
+double orc_shared_gate(int32_t d, int32_t dtype, const void* x_row, const void* w_sg) {
+    double z = 0.0;
+    for (int32_t i = 0; i < d; ++i) z += elem(x_row, dtype, (size_t)i) * elem(w_sg, dtype, (size_t)i);
+    return 1.0 / (1.0 + exp(-z));
+}
+
 int32_t orc_token_output(const orc_cfg_t* c, const void* x_row, const int32_t* idx_t,
                          const double* g_t, const uint8_t* cls_t,
                          const void* const* w13, const void* const* w2,
                          const void* w13s, const void* w2s,
                          const void* const* lA, const void* const* lB,
                          double* out, double* ys, double* yslot) {
+    return orc_token_output_sg(c, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, NULL, lA, lB, out, ys, yslot);
+}
+
+int32_t orc_token_output_sg(const orc_cfg_t* c, const void* x_row, const int32_t* idx_t,
+                            const double* g_t, const uint8_t* cls_t,
+                            const void* const* w13, const void* const* w2,
+                            const void* w13s, const void* w2s, const void* w_sg,
+                            const void* const* lA, const void* const* lB,
+                            double* out, double* ys, double* yslot) {
     const int32_t d = c->d, K = c->top_k;
     double* x = (double*)calloc((size_t)d, sizeof(double));
     double* s = (double*)calloc((size_t)d, sizeof(double));
@@ -208,8 +225,12 @@ int32_t orc_token_output(const orc_cfg_t* c, const void* x_row, const int32_t* i
     int32_t rc = 0;
     for (int32_t j = 0; j < d; ++j) x[j] = elem(x_row, c->dtype, (size_t)j);
 
-    /* the always-active shared block S(x) (Sec. 2.1) */
+    /* the always-active shared block S(x) (Sec. 2.1), with its output gate if given */
     orc_swiglu(d, c->shared_inter, c->dtype, w13s, w2s, x, s);
+    if (w_sg) {
+        const double gs = orc_shared_gate(d, c->dtype, x_row, w_sg);
+        for (int32_t j = 0; j < d; ++j) s[j] *= gs;
+    }
     for (int32_t j = 0; j < d; ++j) out[j] = s[j];
     if (ys)
         for (int32_t j = 0; j < d; ++j) ys[j] = s[j];

@@ -88,6 +88,19 @@ int32_t orc_token_output(const orc_cfg_t* c, const void* x_row, const int32_t* i
                          const void* const* lA, const void* const* lB,
                          double* out, double* ys, double* yslot);
 
+/* The shared block's output gate sigmoid(sum_i x[i] w_sg[i]) for one token: the
+ * Qwen2-style shared expert, whose output is scaled by this gate. */
+double orc_shared_gate(int32_t d, int32_t dtype, const void* x_row, const void* w_sg);
+
+/* orc_token_output with a gated shared block (w_sg [d], nullable): S(x) is
+ * orc_shared_gate(x) SwiGLU_s(x), in the plain term and inside every LoRE slot's S(x) + B A x. */
+int32_t orc_token_output_sg(const orc_cfg_t* c, const void* x_row, const int32_t* idx_t,
+                            const double* g_t, const uint8_t* cls_t,
+                            const void* const* w13, const void* const* w2,
+                            const void* w13s, const void* w2s, const void* w_sg,
+                            const void* const* lA, const void* const* lB,
+                            double* out, double* ys, double* yslot);
+
 /* Exact residual of the CPU path (Sec. 4.3): resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t).
  * Returns 0, or -1 if a needed expert pointer is NULL. */
 int32_t orc_exact_residual(const orc_cfg_t* c, int32_t T, const void* x, const int32_t* idx,
