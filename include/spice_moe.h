@@ -173,6 +173,26 @@ spice_status_t moe_expert_ffn_grouped(const spice_moe_cfg_t* cfg, int32_t T, con
                                       void* ws, size_t ws_bytes, spice_stream_t stream);
 
 /*
+ * Step 3 with a gated shared block (the Qwen2-style shared expert, whose output carries a
+ * sigmoid gate): as moe_expert_ffn_grouped, with
+ *   S(x_t) = sigmoid(w_sg . x_t) SwiGLU_s(x_t),
+ * the dot product taken in fp64.  S is the model's native shared expert of Sec. 4.2, so the
+ * gated S is what y_shared holds and what moe_combine (and the draft update) use, in the
+ * plain shared term and inside every LoRE slot's S(x) + B_e A_e x (Eq. 7 / 11).
+ *   w_shared_gate  device [d] (dtype): the gate's weight row; required when shared_inter > 0
+ * The gate values go to the workspace (its size covers them).  Errors: as
+ * moe_expert_ffn_grouped, plus INVALID for a NULL w_shared_gate.
+ */
+spice_status_t moe_expert_ffn_grouped_gated(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                            const int32_t* perm, const int32_t* offsets,
+                                            const int32_t* resident_slot, const void* w13_pool,
+                                            const void* w2_pool, const void* w13_shared,
+                                            const void* w2_shared, const void* w_shared_gate,
+                                            const void* lore_A, const void* lore_B, float* y_slots,
+                                            float* y_shared, void* ws, size_t ws_bytes,
+                                            spice_stream_t stream);
+
+/*
  * Step 4: LoRE correction delta = B_e (A_e x) (Eq. 9) for every LORE slot, grouped by
  * expert.  The shared part S(x) of Eq. 11 is not recomputed: moe_combine adds it.
  *   lore_A  device [N][r][d] (dtype), lore_B device [N][d][r] (dtype): factors of every

@@ -585,6 +585,7 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
             if (gi < n && dim < a.d) {
                 float* dst = (tile.kind == kKindShared) ? a.y_shared + (size_t)gi * a.d
                                                         : a.y_slots + (size_t)(start + gi) * a.d;
+                if (tile.kind == kKindShared && a.sgate) s *= a.sgate[gi];  // gated shared block
                 *reinterpret_cast<f32x4_t*>(dst + dim) = s;
             }
         }

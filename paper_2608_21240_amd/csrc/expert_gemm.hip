@@ -365,10 +365,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
             }
         } else {
             float* dst = j.shared ? a.y_shared + (size_t)pos * a.d : a.y_slots + (size_t)(j.start + pos) * a.d;
+            const float gs = (j.shared && a.sgate) ? a.sgate[pos] : 1.0f;  // gated shared block
 #pragma unroll
             for (int s = 0; s < 8; ++s) {
                 const int f = j.feat0 + wf * 128 + s * 16 + quad * 4;
-                *reinterpret_cast<f32x4_t*>(dst + f) = acc[s][t];
+                *reinterpret_cast<f32x4_t*>(dst + f) = acc[s][t] * gs;
             }
         }
     }
@@ -431,6 +432,7 @@ hipError_t launch_expert_gemm(const FfnArgs& f, bool hit, bool shared, hipStream
     a.hs = static_cast<uint16_t*>(f.hs);
     a.y_slots = f.y_slots;
     a.y_shared = f.y_shared;
+    a.sgate = f.sgate;
     a.ctrl = f.ctrl;
     if (!hit) a.N = 0;  // no expert tiles
     // upper bound of the tile count: sum_e ceil(n_e / kBT) <= T*K / kBT + min(N, C)

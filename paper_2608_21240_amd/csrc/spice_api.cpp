@@ -125,6 +125,7 @@ WsLayout ws_layout(const spice_moe_cfg_t& c, int32_t T) {
     L.h = off;      off += align256(slots * ((size_t)c.inter + kHPad) * es);
     L.hs = off;     off += align256(t * ((size_t)c.shared_inter + kHPad) * es);
     L.u = off;      off += align256(slots * (size_t)c.lore_rank * sizeof(float));
+    L.sgate = off;  off += align256(t * sizeof(float));
     L.total = off;
     return L;
 }
@@ -228,7 +229,8 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
                               const int32_t* offsets, const int32_t* resident_slot, const void* w13_pool,
                               const void* w2_pool, const void* w13_shared, const void* w2_shared,
                               const void* lore_A, const void* lore_B, float* y_slots, float* y_shared, void* ws,
-                              size_t ws_bytes, spice_stream_t stream, int groups, const char* name) {
+                              size_t ws_bytes, spice_stream_t stream, int groups, const char* name,
+                              const void* w_shared_gate = nullptr) {
     spice_status_t st = check_cfg(cfg);
     if (st != SPICE_OK) return st;
     const spice_moe_cfg_t& c = *cfg;
@@ -271,6 +273,12 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
     a.lore_A = lore_A; a.lore_B = lore_B; a.y_slots = y_slots; a.y_shared = y_shared;
     a.h = wsb + L.h; a.hs = wsb + L.hs; a.u = reinterpret_cast<float*>(wsb + L.u);
     a.ctrl = reinterpret_cast<uint32_t*>(wsb);
+    if (w_shared_gate && (groups & spice::kDoShared) && c.shared_inter > 0) {
+        float* sg = reinterpret_cast<float*>(wsb + L.sgate);
+        hipError_t e = spice::launch_shared_gate(x, w_shared_gate, T, c.d, c.dtype, sg, stream);
+        if (e != hipSuccess) return hip_fail(e, name);
+        a.sgate = sg;
+    }
     hipError_t e = spice::launch_expert_ffn(a, stream);
     if (e != hipSuccess) return hip_fail(e, name);
     return SPICE_OK;
@@ -286,6 +294,23 @@ spice_status_t moe_expert_ffn_grouped(const spice_moe_cfg_t* cfg, int32_t T, con
     if (lore_A && lore_B) groups |= spice::kDoLore;
     return run_ffn(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared, lore_A,
                    lore_B, y_slots, y_shared, ws, ws_bytes, stream, groups, "moe_expert_ffn_grouped");
+    SPICE_TRY_END
+}
+
+spice_status_t moe_expert_ffn_grouped_gated(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                            const int32_t* perm, const int32_t* offsets, const int32_t* resident_slot,
+                                            const void* w13_pool, const void* w2_pool, const void* w13_shared,
+                                            const void* w2_shared, const void* w_shared_gate, const void* lore_A,
+                                            const void* lore_B, float* y_slots, float* y_shared, void* ws,
+                                            size_t ws_bytes, spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    int groups = spice::kDoHit | spice::kDoShared;
+    if (lore_A && lore_B) groups |= spice::kDoLore;
+    if (cfg && cfg->shared_inter > 0 && !w_shared_gate)
+        return fail(SPICE_ERR_INVALID, "moe_expert_ffn_grouped_gated: w_shared_gate is NULL");
+    return run_ffn(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared, lore_A,
+                   lore_B, y_slots, y_shared, ws, ws_bytes, stream, groups, "moe_expert_ffn_grouped_gated",
+                   w_shared_gate);
     SPICE_TRY_END
 }
 

@@ -37,6 +37,7 @@ struct WsLayout {
     size_t h;       // SwiGLU intermediate of routed slots [T*K][I + kHPad] (dtype)
     size_t hs;      // shared-block intermediate [T][I_s + kHPad] (dtype)
     size_t u;       // LoRE A x, fp32 [T*K][r]
+    size_t sgate;   // output gate of the shared block, fp32 [T]
     size_t total;
 };
 WsLayout ws_layout(const spice_moe_cfg_t& c, int32_t T);
@@ -84,6 +85,7 @@ struct FfnArgs {
     const void* lore_B;
     float* y_slots;
     float* y_shared;
+    const float* sgate;  // nullable: y_shared[t] is scaled by sgate[t] (gated shared block)
     void* h;        // workspace [T*K][I]
     void* hs;       // workspace [T][I_s]
     float* u;       // workspace [T*K][r]
@@ -152,6 +154,7 @@ struct GemmArgs {
     uint16_t* hs;
     float* y_slots;
     float* y_shared;
+    const float* sgate;  // nullable, as in FfnArgs
     uint32_t* ctrl;
 };
 
@@ -160,6 +163,9 @@ hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+// sgate[t] = sigmoid(w_sg . x[t]) for T tokens (fp64 dot products), shared_gate.hip.
+hipError_t launch_shared_gate(const void* x, const void* w_sg, int32_t T, int32_t d, int32_t dtype, float* sgate,
+                              hipStream_t s);
 hipError_t launch_expert_ffn_fetched(const FfnArgs& a, const FetchArgs& f, hipStream_t s);
 hipError_t launch_combine(const CombineArgs& a, hipStream_t s);
 hipError_t launch_spec_update(const SpecArgs& a, hipStream_t s);

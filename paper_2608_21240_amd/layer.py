@@ -48,6 +48,7 @@ class HostLayer:
         self.wg = synth.gen_router(wl, layer)
         self.bias = synth.gen_bias(wl, layer)
         self.w13s, self.w2s = synth.gen_shared(wl, layer)
+        self.w_sg = synth.gen_shared_gate(wl, layer)  # None: ungated shared block
         self._experts: Dict[int, tuple] = {}
         self._lore: Dict[int, tuple] = {}
 
@@ -109,6 +110,7 @@ class DeviceLayer:
         self.bias = None if host.bias is None else torch.from_numpy(host.bias).to(device)
         self.w13s = to_tensor(host.w13s, dt, device)
         self.w2s = to_tensor(host.w2s, dt, device)
+        self.w_sg = None if host.w_sg is None else to_tensor(host.w_sg, dt, device)
         slot = np.full(s.n_experts, -1, np.int32)
         host.prefetch(range(s.n_experts) if host_exact else host.resident,
                       range(s.n_experts) if s.lore_rank > 0 else ())
@@ -205,10 +207,15 @@ class LayerRun:
 
     def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
         T = self.T if T is None else T
-        spice.moe_expert_ffn_grouped(self.cfg, T, x, self.perm, self.offsets, L.resident_slot, L.w13_pool,
-                                     L.w2_pool, L.w13s, L.w2s, L.lore_A if fuse_lore else None,
-                                     L.lore_B if fuse_lore else None, self.y_slots, self.y_shared, self.ws,
-                                     self.ws_bytes)
+        la, lb = (L.lore_A, L.lore_B) if fuse_lore else (None, None)
+        if L.w_sg is not None:
+            spice.moe_expert_ffn_grouped_gated(self.cfg, T, x, self.perm, self.offsets, L.resident_slot, L.w13_pool,
+                                               L.w2_pool, L.w13s, L.w2s, L.w_sg, la, lb, self.y_slots,
+                                               self.y_shared, self.ws, self.ws_bytes)
+        else:
+            spice.moe_expert_ffn_grouped(self.cfg, T, x, self.perm, self.offsets, L.resident_slot, L.w13_pool,
+                                         L.w2_pool, L.w13s, L.w2s, la, lb, self.y_slots, self.y_shared, self.ws,
+                                         self.ws_bytes)
 
     def lore(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None):
         T = self.T if T is None else T

@@ -27,7 +27,8 @@ SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
 # Every function the header declares (checked against include/spice_moe.h by the tests).
 EXPORTS = (
     "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
-    "moe_route_bucket", "moe_expert_ffn_grouped", "lore_surrogate_apply", "moe_combine",
+    "moe_route_bucket", "moe_expert_ffn_grouped", "moe_expert_ffn_grouped_gated", "lore_surrogate_apply",
+    "moe_combine",
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
     "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
     "moe_spec_update", "moe_prefetch_h_min", "moe_prefetch_queue", "moe_cache_prefetch",
@@ -93,6 +94,8 @@ def lib() -> ctypes.CDLL:
             "moe_route_bucket": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P,
                                       ctypes.POINTER(spice_host_out_t), _P, _Z, _P]),
             "moe_expert_ffn_grouped": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
+            "moe_expert_ffn_grouped_gated": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _P, _Z,
+                                                  _P]),
             "lore_surrogate_apply": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
             "moe_combine": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
             "moe_exact_residual_host": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I]),
@@ -192,6 +195,14 @@ def moe_expert_ffn_grouped(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2
         ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(resident_slot), _p(w13_pool), _p(w2_pool),
         _p(w13_shared), _p(w2_shared), _p(lore_A), _p(lore_B), _p(y_slots), _p(y_shared), _p(ws), ws_bytes,
         _stream(stream)))
+
+
+def moe_expert_ffn_grouped_gated(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared,
+                                 w_shared_gate, lore_A, lore_B, y_slots, y_shared, ws, ws_bytes, stream=None) -> None:
+    _check("moe_expert_ffn_grouped_gated", lib().moe_expert_ffn_grouped_gated(
+        ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(resident_slot), _p(w13_pool), _p(w2_pool),
+        _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(y_slots), _p(y_shared),
+        _p(ws), ws_bytes, _stream(stream)))
 
 
 def lore_surrogate_apply(cfg, T, x, perm, offsets, lore_A, lore_B, y_slots, ws, ws_bytes, stream=None) -> None:

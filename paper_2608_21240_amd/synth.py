@@ -27,7 +27,7 @@ from .workloads import DTYPE_BF16, DTYPE_F32, Workload
 
 WEIGHT_STD = 0.02
 
-T_X, T_WG, T_POP, T_CONF, T_W13, T_W2, T_W13S, T_W2S, T_LA, T_LB, T_RES = range(1, 12)
+T_X, T_WG, T_POP, T_CONF, T_W13, T_W2, T_W13S, T_W2S, T_LA, T_LB, T_RES, T_SG = range(1, 13)
 
 
 def _wid(wl: Workload) -> int:
@@ -144,6 +144,13 @@ def gen_shared(wl: Workload, layer: int = 0) -> Tuple[np.ndarray, np.ndarray]:
     w13 = _normal(_key(wl, layer, T_W13S), (2 * s.shared_inter, s.d), WEIGHT_STD, s.dtype)
     w2 = _normal(_key(wl, layer, T_W2S), (s.d, s.shared_inter), WEIGHT_STD, s.dtype)
     return w13, w2
+
+
+def gen_shared_gate(wl: Workload, layer: int = 0) -> Optional[np.ndarray]:
+    """Gate row w_sg[d] ~ N(0, 0.02) of a gated shared block, or None when ungated."""
+    if not wl.shared_gate:
+        return None
+    return _normal(_key(wl, layer, T_SG), (wl.shape.d,), WEIGHT_STD, wl.shape.dtype)
 
 
 def gen_lore(wl: Workload, layer: int, e: int) -> Tuple[np.ndarray, np.ndarray]:

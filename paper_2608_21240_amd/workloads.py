@@ -63,6 +63,7 @@ class Workload:
     tau: float = 0.5
     conf_mode: int = CONF_INPUT
     norm_topk: int = 0
+    shared_gate: bool = False  # sigmoid output gate on the shared block (Qwen2-style shared expert)
     zipf_s: float = 1.1
     seed: int = 0
     layers: int = 1
@@ -89,6 +90,9 @@ WORKLOADS = {
     "dsv2_stack": Workload("dsv2_stack", DSV2, tokens=64, resident=24, skew=False, layers=26,
                            cache_slots=24, steps=128),
     "qwen2_prefill": Workload("qwen2_prefill", QWEN2, tokens=4096, resident=64, skew=True),
+    # the same layers with the shared block's sigmoid output gate of the released model
+    "qwen2_gated_decode_r32": Workload("qwen2_gated_decode_r32", QWEN2, tokens=16, resident=32, skew=True,
+                                       shared_gate=True),
 }
 
 

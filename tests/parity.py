@@ -107,7 +107,7 @@ class Case:
         out = np.empty((len(toks), s.d)); ys = np.empty((len(toks), s.d)); yslot = np.empty((len(toks), s.top_k, s.d))
         for i, t in enumerate(toks):
             out[i], ys[i], yslot[i] = orc.token_output(cfg, self.x[t], r["idx"][t], r["g"][t], r["cls"][t], w13, w2,
-                                                       self.host.w13s, self.host.w2s, la, lb)
+                                                       self.host.w13s, self.host.w2s, la, lb, self.host.w_sg)
         r.update(out=out, y_shared=ys, y_slot=yslot, tokens=np.array(toks))
         exact_e = sorted(set(r["idx"][toks][r["cls"][toks] == EXACT].tolist()))
         e13, e2, _, _ = self.host.tables(exact_e, [])

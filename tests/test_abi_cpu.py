@@ -112,6 +112,23 @@ def test_ffn_lore_combine_validation():
     assert st == spice.SPICE_ERR_INVALID
 
 
+def test_gated_ffn_validation():
+    c = cfg()
+    L = spice.lib()
+    ws = spice.spice_workspace_bytes(c, 4)
+    # the gate row is required when the layer has a shared block
+    st = L.moe_expert_ffn_grouped_gated(ctypes.byref(c), 4, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY, DUMMY,
+                                        None, None, None, 0x100000, 0x900000, DUMMY, ws, None)
+    assert st == spice.SPICE_ERR_INVALID
+    assert "w_shared_gate" in spice.last_error()
+    # and the usual checks still apply (missing pools)
+    st = L.moe_expert_ffn_grouped_gated(ctypes.byref(c), 4, DUMMY, DUMMY, DUMMY, DUMMY, None, None, DUMMY, DUMMY,
+                                        DUMMY, None, None, 0x100000, 0x900000, DUMMY, ws, None)
+    assert st == spice.SPICE_ERR_INVALID
+    # the workspace holds the gate values: one fp32 per token beyond the ungated layout
+    assert spice.spice_workspace_bytes(c, 64) >= spice.spice_workspace_bytes(c, 4) + 60 * 4
+
+
 def test_status_strings():
     assert spice.spice_status_string(spice.SPICE_ERR_WORKSPACE) == "SPICE_ERR_WORKSPACE"
     assert spice.spice_status_string(12345) == "unknown spice_status_t"

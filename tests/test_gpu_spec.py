@@ -46,7 +46,8 @@ def _views(shape, ws):
         vs.append(SimpleNamespace(wg=LY.to_tensor(w["wg"], dt, "cuda"), bias=None,
                                   w13s=LY.to_tensor(w["w13s"], dt, "cuda"), w2s=LY.to_tensor(w["w2s"], dt, "cuda"),
                                   lore_A=A if A is not None else torch.zeros((shape.n_experts, r, shape.d)).cuda(),
-                                  lore_B=B if B is not None else torch.zeros((shape.n_experts, shape.d, r)).cuda()))
+                                  lore_B=B if B is not None else torch.zeros((shape.n_experts, shape.d, r)).cuda(),
+                                  w_sg=None))
     return vs
 
 
