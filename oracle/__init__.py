@@ -53,12 +53,20 @@ class Cfg(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
                 ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32), ("conf_mode", ctypes.c_int32),
-                ("tau", ctypes.c_float)]
+                ("tau", ctypes.c_float), ("wfmt", ctypes.c_int32)]
 
 
-def make_cfg(shape, tau: float = 0.5, conf_mode: int = CONF_INPUT, norm_topk: int = 0) -> Cfg:
+MXFP4 = 2  # routed experts' weights as MXFP4 blobs (see spice_oracle.h)
+
+
+def make_cfg(shape, tau: float = 0.5, conf_mode: int = CONF_INPUT, norm_topk: int = 0, wfmt: int = 0) -> Cfg:
     return Cfg(shape.d, shape.n_experts, shape.top_k, shape.inter, shape.shared_inter,
-               shape.lore_rank, shape.dtype, norm_topk, conf_mode, tau)
+               shape.lore_rank, shape.dtype, norm_topk, conf_mode, tau, wfmt)
+
+
+def expert_dtype(cfg: Cfg) -> int:
+    """Storage of the routed experts' weights: the cfg dtype, or MXFP4."""
+    return MXFP4 if cfg.wfmt == MXFP4 else cfg.dtype
 
 
 _P = ctypes.c_void_p
@@ -80,6 +88,8 @@ def _declare(L: ctypes.CDLL) -> None:
     L.orc_token_output_sg.restype = _I
     L.orc_shared_gate.argtypes = [_I, _I, _P, _P]
     L.orc_shared_gate.restype = ctypes.c_double
+    L.orc_mxfp4_elem.argtypes = [_P, _I, _I, _I, _I]
+    L.orc_mxfp4_elem.restype = ctypes.c_double
     L.orc_exact_residual.argtypes = [cp, _I, _P, _P, _P, _P, _P, _P, _P]
     L.orc_exact_residual.restype = _I
     L.orc_lru_step.argtypes = [_I, _I, _P, _P, _I, _I, _I, _P, _P, _I, _P, _P]
@@ -106,6 +116,8 @@ def _c(a, dtype) -> np.ndarray:
 
 
 def _store(a: np.ndarray, dtype: int) -> np.ndarray:
+    if dtype == MXFP4:
+        return _c(a, np.uint8)
     return _c(a, np.uint16 if dtype == 1 else np.float32)
 
 
@@ -160,6 +172,11 @@ def bucket(cfg: Cfg, idx, cls):
     return offsets, perm, inv, counts
 
 
+def mxfp4_elem(blob, rows: int, K: int, r: int, c: int) -> float:
+    b = _c(blob, np.uint8)
+    return lib().orc_mxfp4_elem(_ptr(b), rows, K, r, c)
+
+
 def swiglu(d: int, inter: int, dtype: int, w13, w2, x64):
     w13, w2 = _store(w13, dtype), _store(w2, dtype)
     x64 = _c(x64, np.float64); y = np.empty(d)
@@ -185,7 +202,7 @@ def token_output(cfg: Cfg, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, lA, lB,
     w_sg: the shared block's gate vector [d], or None for an ungated shared block."""
     x_row = _store(x_row, cfg.dtype)
     idx_t = _c(idx_t, np.int32); g_t = _c(g_t, np.float64); cls_t = _c(cls_t, np.uint8)
-    t13, k1 = _table(w13, cfg.dtype); t2, k2 = _table(w2, cfg.dtype)
+    t13, k1 = _table(w13, expert_dtype(cfg)); t2, k2 = _table(w2, expert_dtype(cfg))
     tA, k3 = _table(lA, cfg.dtype); tB, k4 = _table(lB, cfg.dtype)
     s13, s2 = _store(w13s, cfg.dtype), _store(w2s, cfg.dtype)
     sg = None if w_sg is None else _store(w_sg, cfg.dtype)
@@ -201,7 +218,7 @@ def token_output(cfg: Cfg, x_row, idx_t, g_t, cls_t, w13, w2, w13s, w2s, lA, lB,
 def exact_residual(cfg: Cfg, x, idx, g, cls, w13, w2):
     T = x.shape[0]
     x = _store(x, cfg.dtype); idx = _c(idx, np.int32); g = _c(g, np.float64); cls = _c(cls, np.uint8)
-    t13, k1 = _table(w13, cfg.dtype); t2, k2 = _table(w2, cfg.dtype)
+    t13, k1 = _table(w13, expert_dtype(cfg)); t2, k2 = _table(w2, expert_dtype(cfg))
     resid = np.empty((T, cfg.d))
     rc = lib().orc_exact_residual(ctypes.byref(cfg), T, _ptr(x), _ptr(idx), _ptr(g), _ptr(cls), t13, t2,
                                   _ptr(resid))

@@ -34,6 +34,29 @@ static double elem(const void* p, int32_t dtype, size_t i) {
     return (double)((const float*)p)[i];
 }
 
+/* FP4 E2M1 code (OCP MX v1.0): sign bit 3, exponent bits 2..1 (bias 1), mantissa bit 0;
+ * exponent 0 is subnormal (0 or 0.5).  Magnitudes 0, 0.5, 1, 1.5, 2, 3, 4, 6. */
+static double e2m1(unsigned code) {
+    const unsigned e = (code >> 1) & 3u, m = code & 1u;
+    const double mag = (e == 0) ? 0.5 * m : ldexp(1.0 + 0.5 * m, (int)e - 1);
+    return (code & 8u) ? -mag : mag;
+}
+
+double orc_mxfp4_elem(const void* blob, int32_t rows, int32_t K, int32_t r, int32_t c) {
+    const uint8_t* b = (const uint8_t*)blob;
+    const uint8_t byte = b[(size_t)r * (K / 2) + c / 2];
+    const unsigned code = (c & 1) ? (byte >> 4) : (byte & 15u);
+    const uint8_t s = b[(size_t)rows * (K / 2) + (size_t)r * (K / 32) + c / 32];
+    if (s == 255) return NAN; /* E8M0 NaN */
+    return ldexp(e2m1(code), (int)s - 127);
+}
+
+/* Weight (r, c) of a [rows][K] matrix in storage dtype (fp32, bf16 or an MXFP4 blob). */
+static double welem(const void* p, int32_t dtype, int32_t rows, int32_t K, int32_t r, int32_t c) {
+    if (dtype == ORC_MXFP4) return orc_mxfp4_elem(p, rows, K, r, c);
+    return elem(p, dtype, (size_t)r * K + c);
+}
+
 /* Eq. 1: the router maps the hidden state to one logit per routed expert. */
 void orc_router_logits(const orc_cfg_t* c, int32_t T, const void* x, const void* wg,
                        const float* bias, double* z, double* zabs) {
@@ -165,14 +188,14 @@ void orc_swiglu(int32_t d, int32_t inter, int32_t dtype, const void* w13, const 
     for (int32_t i = 0; i < inter; ++i) {
         double a = 0.0, b = 0.0;
         for (int32_t j = 0; j < d; ++j) {
-            a += elem(w13, dtype, (size_t)i * d + j) * x[j];
-            b += elem(w13, dtype, (size_t)(inter + i) * d + j) * x[j];
+            a += welem(w13, dtype, 2 * inter, d, i, j) * x[j];
+            b += welem(w13, dtype, 2 * inter, d, inter + i, j) * x[j];
         }
         h[i] = silu(a) * b;
     }
     for (int32_t j = 0; j < d; ++j) {
         double acc = 0.0;
-        for (int32_t i = 0; i < inter; ++i) acc += elem(w2, dtype, (size_t)j * inter + i) * h[i];
+        for (int32_t i = 0; i < inter; ++i) acc += welem(w2, dtype, d, inter, j, i) * h[i];
         y[j] = acc;
     }
     free(h);
@@ -246,7 +269,7 @@ int32_t orc_token_output_sg(const orc_cfg_t* c, const void* x_row, const int32_t
         } else {
             /* resident hit, or exact miss served with the same expert weights */
             if (!w13[e] || !w2[e]) { rc = -1; break; }
-            orc_swiglu(d, c->inter, c->dtype, w13[e], w2[e], x, y);
+            orc_swiglu(d, c->inter, c->wfmt == ORC_MXFP4 ? ORC_MXFP4 : c->dtype, w13[e], w2[e], x, y);
             for (int32_t j = 0; j < d; ++j) out[j] += gk * y[j];
         }
         if (yslot)
@@ -274,7 +297,7 @@ int32_t orc_exact_residual(const orc_cfg_t* c, int32_t T, const void* x, const i
             size_t s = (size_t)t * K + k;
             if (cls[s] != ORC_EXACT) continue;
             if (!w13[idx[s]] || !w2[idx[s]]) { rc = -1; break; }
-            orc_swiglu(d, c->inter, c->dtype, w13[idx[s]], w2[idx[s]], xr, y);
+            orc_swiglu(d, c->inter, c->wfmt == ORC_MXFP4 ? ORC_MXFP4 : c->dtype, w13[idx[s]], w2[idx[s]], xr, y);
             for (int32_t j = 0; j < d; ++j) resid[(size_t)t * d + j] += g[s] * y[j];
         }
     }

@@ -17,6 +17,12 @@
  *   shared   W13s[2Is][d], W2s[d][Is]
  *   LoRE     A   [r][d],  B [d][r]          (Eq. 9)
  * Slot id of token t's k-th routed choice = t*K + k.
+ *
+ * MXFP4 weights (routed experts when cfg.wfmt == ORC_MXFP4, OCP Microscaling formats v1.0):
+ * a [rows][K] matrix (K a multiple of 32) is one byte blob: rows*K/2 bytes of FP4 E2M1
+ * codes, row-major, element 2i in the low nibble of byte i and 2i+1 in the high nibble;
+ * then rows*K/32 bytes of E8M0 block scales, row-major, one per 32 consecutive elements
+ * of a row.  Element value = 2^(scale - 127) * e2m1(code).  W13 is [2I][d], W2 [d][I].
  * Parity pins: see tests/test_oracle_*.py.  No function here is unpinned.
  * Speculative prefetching (Alg. 1) uses an identity stand-in for the target layer's
  * attention: this oracle covers the MoE part of the draft update only.
@@ -30,7 +36,7 @@
 extern "C" {
 #endif
 
-enum { ORC_F32 = 0, ORC_BF16 = 1 };
+enum { ORC_F32 = 0, ORC_BF16 = 1, ORC_MXFP4 = 2 };
 enum { ORC_HIT = 0, ORC_LORE = 1, ORC_EXACT = 2 };
 enum { ORC_CONF_INPUT = 0, ORC_CONF_GATE = 1, ORC_CONF_GATE_RENORM = 2 };
 
@@ -40,6 +46,7 @@ typedef struct {
     int32_t norm_topk; /* 1: divide the K selected gates by their sum */
     int32_t conf_mode; /* ORC_CONF_* */
     float tau;         /* confidence threshold */
+    int32_t wfmt;      /* routed experts' weight format: 0 = the cfg dtype, ORC_MXFP4 = MXFP4 blobs */
 } orc_cfg_t;
 
 /* Router logits z[t][e] = sum_i x[t][i] Wg[e][i] + bias[e] (Eq. 1).  zabs (nullable)
@@ -68,7 +75,8 @@ void orc_classify(const orc_cfg_t* c, int32_t T, const int32_t* idx, const int32
 void orc_bucket(const orc_cfg_t* c, int32_t T, const int32_t* idx, const uint8_t* cls,
                 int32_t* offsets, int32_t* perm, int32_t* inv_perm, int32_t* counts);
 
-/* One SwiGLU FFN on one token: y = W2 (silu(W1 x) * (W3 x)), x given in double. */
+/* One SwiGLU FFN on one token: y = W2 (silu(W1 x) * (W3 x)), x given in double.  dtype is
+ * the weights' storage: ORC_F32, ORC_BF16 or ORC_MXFP4 (blobs as described above). */
 void orc_swiglu(int32_t d, int32_t inter, int32_t dtype, const void* w13, const void* w2,
                 const double* x, double* y);
 
@@ -100,6 +108,9 @@ int32_t orc_token_output_sg(const orc_cfg_t* c, const void* x_row, const int32_t
                             const void* w13s, const void* w2s, const void* w_sg,
                             const void* const* lA, const void* const* lB,
                             double* out, double* ys, double* yslot);
+
+/* One MXFP4 element (r, c) of a [rows][K] blob, widened to double (exact). */
+double orc_mxfp4_elem(const void* blob, int32_t rows, int32_t K, int32_t r, int32_t c);
 
 /* Exact residual of the CPU path (Sec. 4.3): resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t).
  * Returns 0, or -1 if a needed expert pointer is NULL. */

@@ -23,7 +23,7 @@ from typing import List, Optional, Tuple
 
 import numpy as np
 
-from .workloads import DTYPE_BF16, DTYPE_F32, Workload
+from .workloads import DTYPE_BF16, DTYPE_F32, WFMT_MXFP4, Workload
 
 WEIGHT_STD = 0.02
 
@@ -130,9 +130,50 @@ def gen_conf(wl: Workload, layer: int = 0, step: int = 0, tokens: Optional[int] 
     return rng(wl.seed, _wid(wl), layer, T_CONF, step, T).random((T, wl.shape.top_k), dtype=np.float32)
 
 
+# FP4 E2M1 magnitudes by code 0..7 (OCP Microscaling formats v1.0); the sign is bit 3.
+E2M1_MAGNITUDES = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+
+
+def quantize_mxfp4(a: np.ndarray) -> np.ndarray:
+    """A [rows][K] fp32 matrix (K a multiple of 32) -> one MXFP4 byte blob: rows*K/2 bytes of
+    E2M1 codes (element 2i in the low nibble of byte i), then rows*K/32 E8M0 block scales.
+
+    Per block of 32 the shared exponent is floor(log2(max |a|)) - 2 (2 = the largest E2M1
+    exponent); elements a / 2^exponent go to the nearest E2M1 value, ties to the even code,
+    saturating at 6.  An all-zero block gets scale 2^0."""
+    rows, K = a.shape
+    assert K % 32 == 0
+    blk = np.asarray(a, np.float64).reshape(rows, K // 32, 32)
+    amax = np.abs(blk).max(axis=2)
+    with np.errstate(divide="ignore"):
+        ex = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))) - 2, 0).astype(np.int64)
+    ex = np.clip(ex, -127, 127)
+    q = np.abs(blk) / np.ldexp(1.0, ex)[:, :, None]
+    dist = np.abs(q[..., None] - E2M1_MAGNITUDES)  # [rows][blocks][32][8]
+    best = dist.min(axis=-1, keepdims=True)
+    tie_ok = dist == best
+    # among equally near codes take the even one (the larger code when q saturates above 6)
+    even = (np.arange(8) % 2 == 0)
+    pick = np.where(tie_ok & even, np.arange(8), -1).max(axis=-1)
+    pick = np.where(pick >= 0, pick, np.argmax(tie_ok, axis=-1))
+    codes = (pick | np.where((blk < 0) & (pick > 0), 8, 0)).astype(np.uint8).reshape(rows, K)
+    packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    scales = (ex + 127).astype(np.uint8)
+    return np.concatenate([packed.reshape(-1), scales.reshape(-1)])
+
+
+def mxfp4_bytes(rows: int, K: int) -> int:
+    return rows * K // 2 + rows * K // 32
+
+
 def gen_expert(wl: Workload, layer: int, e: int) -> Tuple[np.ndarray, np.ndarray]:
-    """Routed expert e: w13[2I][d] (rows 0..I-1 gate W1, rows I..2I-1 up W3), w2[d][I]."""
+    """Routed expert e: w13[2I][d] (rows 0..I-1 gate W1, rows I..2I-1 up W3), w2[d][I] in the
+    storage dtype, or as MXFP4 blobs (quantize_mxfp4 of the same draws) when wl.wfmt is MXFP4."""
     s = wl.shape
+    if wl.wfmt == WFMT_MXFP4:
+        w13 = rng(*_key(wl, layer, T_W13, e)).standard_normal(size=(2 * s.inter, s.d), dtype=np.float32)
+        w2 = rng(*_key(wl, layer, T_W2, e)).standard_normal(size=(s.d, s.inter), dtype=np.float32)
+        return quantize_mxfp4(w13 * np.float32(WEIGHT_STD)), quantize_mxfp4(w2 * np.float32(WEIGHT_STD))
     w13 = _normal(_key(wl, layer, T_W13, e), (2 * s.inter, s.d), WEIGHT_STD, s.dtype)
     w2 = _normal(_key(wl, layer, T_W2, e), (s.d, s.inter), WEIGHT_STD, s.dtype)
     return w13, w2

@@ -11,6 +11,7 @@ from typing import Optional, Tuple
 
 DTYPE_F32 = 0
 DTYPE_BF16 = 1
+WFMT_MXFP4 = 2  # routed experts' weights as OCP MXFP4 (E2M1 elements, E8M0 scale per 32)
 
 CONF_INPUT = 0
 CONF_GATE = 1
@@ -64,6 +65,7 @@ class Workload:
     conf_mode: int = CONF_INPUT
     norm_topk: int = 0
     shared_gate: bool = False  # sigmoid output gate on the shared block (Qwen2-style shared expert)
+    wfmt: int = 0  # routed experts' weight format: 0 = the shape's dtype, WFMT_MXFP4
     zipf_s: float = 1.1
     seed: int = 0
     layers: int = 1
