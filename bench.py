@@ -76,6 +76,9 @@ def parse():
                    help="exact-miss split (Eq. 12): auto = calibrate the cost model on this host and let the "
                         "planner fetch experts to the GPU when that beats all-CPU; off = all-CPU")
     p.add_argument("--fetch-slots", type=int, default=8, help="fetch pool slots for the exact-miss split")
+    p.add_argument("--weights", default="bf16", choices=("bf16", "mxfp4"),
+                   help="dsv2_decode: routed experts' weights in bf16 (default) or MXFP4 (E2M1 + an E8M0 scale "
+                        "per 32; the exact-miss split then stays off)")
     return p.parse_args()
 
 
@@ -93,7 +96,17 @@ def recorded_traffic():
                        + TRAFFIC_RECORD["write_kib_per_call"] * TRAFFIC_RECORD["write_factor"]))
 
 
-def algorithmic_bytes(shape, idx, cls):
+def expert_bytes(wl) -> int:
+    """HBM bytes of one routed expert in the workload's weight format."""
+    from paper_2608_21240_amd import synth, workloads as W
+
+    s = wl.shape
+    if wl.wfmt == W.WFMT_MXFP4:
+        return synth.mxfp4_bytes(2 * s.inter, s.d) + synth.mxfp4_bytes(s.d, s.inter)
+    return s.expert_bytes
+
+
+def algorithmic_bytes(shape, idx, cls, e_bytes=None):
     """Bytes the method must move on the GPU for one layer call, by kernel.
 
     ffn: distinct HIT experts x expert bytes + shared block + distinct LoRE experts x
@@ -105,7 +118,8 @@ def algorithmic_bytes(shape, idx, cls):
     lore_e = len(set(idx[cls == 1].tolist()))
     n_hit, n_lore = int((cls == 0).sum()), int((cls == 1).sum())
     x_b = T * d * wb
-    ffn = (hit_e * shape.expert_bytes + shape.shared_bytes + lore_e * shape.lore_bytes + x_b
+    eb = shape.expert_bytes if e_bytes is None else e_bytes
+    ffn = (hit_e * eb + shape.shared_bytes + lore_e * shape.lore_bytes + x_b
            + (n_hit + n_lore) * d * 4 + T * d * 4)
     route = shape.n_experts * d * wb + x_b
     combine = (n_hit + n_lore) * d * 4 + 2 * T * d * 4 + T * d * wb
@@ -132,7 +146,9 @@ def main():
     if args.workload == "lore_fit":
         return lore_fit_main(args)
     batches = [int(b) for b in args.batches.split(",")]
-    wl = W.WORKLOADS["dsv2_decode_t32"]
+    wl = W.WORKLOADS["dsv2_decode_mxfp4_t32" if args.weights == "mxfp4" else "dsv2_decode_t32"]
+    if args.weights == "mxfp4":
+        args.split = "off"  # the fetched-expert split copies and runs bf16 experts only
     shape = wl.shape
     t_gen = time.time()
     hosts, devs = [], []
@@ -147,7 +163,8 @@ def main():
     results = {}
     split_info = {}
     for T in batches:
-        run = LY.LayerRun(shape, T, devs[0].C, tau=wl.tau, fetch_slots=args.fetch_slots if args.split == "auto" else 0)
+        run = LY.LayerRun(shape, T, devs[0].C, tau=wl.tau, fetch_slots=args.fetch_slots if args.split == "auto" else 0,
+                          wfmt=wl.wfmt)
         xs = [LY.to_tensor(synth.gen_x(wl, i, 0, T), shape.dtype, "cuda") for i in range(args.instances)]
         confs = [torch.from_numpy(synth.gen_conf(wl, i, 0, T)).cuda() for i in range(args.instances)]
         # per-instance class counts (fixed inputs per instance) from one untimed call
@@ -156,7 +173,7 @@ def main():
             run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
             torch.cuda.synchronize()
             per_inst.append(algorithmic_bytes(shape, run.idx_host[:T].numpy().copy(),
-                                              run.cls_host[:T].numpy().copy()))
+                                              run.cls_host[:T].numpy().copy(), expert_bytes(wl)))
         for w in range(args.warmup):
             i = w % args.instances
             run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
@@ -223,20 +240,24 @@ def main():
         del run
 
     head = results[batches[-1]]
+    mx = args.weights == "mxfp4"
     line = {
         "metric": METRIC, "value": round(head["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(head["ms_per_step"], 4),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
         "data": "synthetic (seeded random-init DSV2-Lite-shaped layers, Zipf(1.1) residency, conf~U(0,1))",
-        "config": {"workload": f"dsv2_lite_moe_layer_decode_T{head['T']}", "hidden": shape.d,
+        "config": {"workload": f"dsv2_lite_moe_layer_decode_T{head['T']}" + ("_mxfp4" if mx else ""),
+                   "expert_weights": args.weights, "hidden": shape.d,
                    "experts": shape.n_experts, "top_k": shape.top_k, "inter": shape.inter,
                    "shared_inter": shape.shared_inter, "lore_rank": shape.lore_rank, "resident": wl.resident,
                    "tau": wl.tau, "tokens": head["T"], "layer_instances": args.instances,
                    "host_threads": args.threads or os.cpu_count()},
-        "roofline": {"bound": "hbm", "kernel": "grouped expert FFN call: ffn_up_kernel + ffn_down_kernel "
-                                               "(moe_expert_ffn_grouped with LoRE fused)",
+        "roofline": {"bound": "hbm", "kernel": "grouped expert FFN call: " + (
+                         "ffn_up_mx_kernel + ffn_down_mx_kernel" if mx else "ffn_up_kernel + ffn_down_kernel") +
+                     " (moe_expert_ffn_grouped with LoRE fused)",
                      "achieved": round(head["ffn_launch_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(head["ffn_launch_GBps"] / HBM_PEAK_GBS, 4), "traffic": recorded_traffic(),
+                     "frac": round(head["ffn_launch_GBps"] / HBM_PEAK_GBS, 4),
+                     "traffic": None if mx else recorded_traffic(),
                      "bytes_per_launch": int(head["ffn_launch_bytes"]), "avg_launch_us": round(head["ffn_launch_us"], 2),
                      "in_step_us": round(head["ffn_us"], 2)},
         "gpu_path": {"tokens_per_s": round(head["gpu_tokens_per_s"], 1), "ms_per_step": round(head["gpu_ms_per_step"], 4),
@@ -267,7 +288,7 @@ def time_ffn_launches(devs, xs, confs, per_inst, shape, wl, T, args, reps: int =
 
     runs = []
     for i, dev in enumerate(devs):
-        r = LY.LayerRun(shape, T, dev.C, tau=wl.tau)
+        r = LY.LayerRun(shape, T, dev.C, tau=wl.tau, wfmt=wl.wfmt)
         r.route(dev, xs[i], confs[i], T, to_host=False)
         runs.append(r)
     for _ in range(2):
@@ -561,7 +582,7 @@ def cpu_baseline(wl, host, budget_s):
     from paper_2608_21240_amd import synth
 
     s = wl.shape
-    cfg = orc.make_cfg(s, tau=wl.tau)
+    cfg = orc.make_cfg(s, tau=wl.tau, wfmt=wl.wfmt)
     w13, w2, la, lb = host.tables(range(s.n_experts), range(s.n_experts))
     tokens = 0
     steps = 0

@@ -88,7 +88,22 @@ typedef struct {
     int32_t norm_topk;    /* 1: renormalise the K selected gates to sum 1 */
     int32_t conf_mode;    /* SPICE_CONF_* */
     float tau;            /* confidence threshold: LoRE iff conf < tau (NaN conf -> exact) */
+    int32_t wfmt;         /* routed experts' weight format: SPICE_WFMT_DTYPE or SPICE_WFMT_MXFP4 */
 } spice_moe_cfg_t;
+
+/* Weight formats of the routed experts (the pool slots and the host copies).
+ * SPICE_WFMT_DTYPE: the cfg dtype, W13 [2I][d] and W2 [d][I] row-major.
+ * SPICE_WFMT_MXFP4: OCP Microscaling MXFP4 (quantised expert weights; the paper runs one of
+ *   its models with 5-bit weights of an unnamed layout).  A [rows][K] matrix is one byte
+ *   blob: rows*K/2 bytes of FP4 E2M1 codes, row-major, element 2i in the low nibble of byte
+ *   i and 2i+1 in the high one; then rows*K/32 bytes of E8M0 scales, row-major, one per 32
+ *   consecutive elements of a row; element value = 2^(scale - 127) * e2m1(code).  A W13 blob
+ *   holds [2I][d] (2I*d*17/32 bytes), a W2 blob [d][I] (d*I*17/32 bytes); a pool slot is one
+ *   such blob.  Needs dtype SPICE_BF16 (activations, router, shared block and LoRE factors
+ *   stay bf16) and d, inter multiples of 32.  The fetched-expert split (moe_split_plan,
+ *   moe_fetch_experts, moe_expert_ffn_fetched) and moe_lore_fit return UNSUPPORTED for it;
+ *   at any T the expert FFN runs on the streaming kernels, not the prefill GEMMs. */
+enum { SPICE_WFMT_DTYPE = 0, SPICE_WFMT_MXFP4 = 2 };
 
 /* Size alignment required: d, inter and shared_inter multiples of 8 (bf16) or 4 (fp32);
  * lore_rank a multiple of 8 (bf16) or 4 (fp32). */

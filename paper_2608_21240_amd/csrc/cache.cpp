@@ -30,6 +30,7 @@
 #include <vector>
 
 #include "spice_moe.h"
+#include "spice_internal.h"
 
 namespace spice {
 spice_status_t set_error(spice_status_t st, const char* msg);
@@ -158,9 +159,8 @@ spice_status_t moe_cache_create(const spice_moe_cfg_t* cfg, int32_t n_layers, co
         c->L = n_layers;
         c->N = N;
         c->C = C;
-        const size_t es = cfg->dtype == SPICE_BF16 ? 2 : 4;
-        c->bytes13 = (size_t)2 * cfg->inter * cfg->d * es;
-        c->bytes2 = (size_t)cfg->d * cfg->inter * es;
+        c->bytes13 = spice::expert_w13_bytes(*cfg);
+        c->bytes2 = spice::expert_w2_bytes(*cfg);
         c->device = device;
         c->slot_expert.assign(initial_experts, initial_experts + (size_t)n_layers * C);
         c->last_use.assign((size_t)n_layers * C, -1);

@@ -1,4 +1,5 @@
 // Exact CPU residual for exact-miss slots (Sec. 4.3: the M_cpu part of Eq. 12).
+// Expert weights are in the cfg dtype, or MXFP4 blobs (cfg.wfmt), decoded on the fly.
 //
 // resid[t] = sum_{k in EXACT(t)} g[t][k] * W2_e (silu(W1_e x_t) * (W3_e x_t)),
 // computed from host-resident expert weights.  Work is grouped by expert so each
@@ -180,6 +181,66 @@ DotsFn pick_dots() {
     return dots_generic;
 }
 
+// ---- MXFP4 rows (OCP MX): 32-element blocks of E2M1 codes (low nibble first) and one
+// E8M0 scale each.  out[j] = sum_i w[i] * xs[j*ld + i], len a multiple of 32.
+const float kE2M1[16] = {0.0f, 0.5f, 1.0f, 1.5f, 2.0f, 3.0f, 4.0f, 6.0f,
+                         -0.0f, -0.5f, -1.0f, -1.5f, -2.0f, -3.0f, -4.0f, -6.0f};
+
+inline float e8m0(uint8_t s) { return s == 255 ? std::nanf("") : std::ldexp(1.0f, (int)s - 127); }
+
+void dots_mx_generic(const uint8_t* el, const uint8_t* sc, size_t len, const float* xs, size_t ld, int n,
+                     float* out) {
+    for (int j = 0; j < n; ++j) {
+        float acc = 0.0f;
+        for (size_t b = 0; b < len / 32; ++b) {
+            const float s = e8m0(sc[b]);
+            float blk = 0.0f;
+            for (int i = 0; i < 16; ++i) {
+                const uint8_t v = el[b * 16 + i];
+                blk += kE2M1[v & 15] * xs[j * ld + b * 32 + 2 * i] + kE2M1[v >> 4] * xs[j * ld + b * 32 + 2 * i + 1];
+            }
+            acc += s * blk;
+        }
+        out[j] = acc;
+    }
+}
+
+// Each block is decoded once (table permute of the 32 codes, times the scale) and used for
+// up to 8 tokens.
+__attribute__((target("avx512f,avx512bw,avx512vl,fma"))) void dots_mx_avx512(const uint8_t* el, const uint8_t* sc,
+                                                                               size_t len, const float* xs,
+                                                                               size_t ld, int n, float* out) {
+    const __m512 lut = _mm512_loadu_ps(kE2M1);
+    const __m128i low4 = _mm_set1_epi8(0x0F);
+    for (int j0 = 0; j0 < n; j0 += 8) {
+        const int nb = std::min(8, n - j0);
+        __m512 acc[8];
+        for (int q = 0; q < 8; ++q) acc[q] = _mm512_setzero_ps();
+        for (size_t b = 0; b < len / 32; ++b) {
+            const __m128i bytes = _mm_loadu_si128(reinterpret_cast<const __m128i*>(el + b * 16));
+            const __m128i lo = _mm_and_si128(bytes, low4), hi = _mm_and_si128(_mm_srli_epi16(bytes, 4), low4);
+            const __m512 s = _mm512_set1_ps(e8m0(sc[b]));
+            const __m512 w0 = _mm512_mul_ps(_mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpacklo_epi8(lo, hi)), lut), s);
+            const __m512 w1 = _mm512_mul_ps(_mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpackhi_epi8(lo, hi)), lut), s);
+            for (int q = 0; q < 8; ++q)
+                if (q < nb) {
+                    const float* x = xs + (size_t)(j0 + q) * ld + b * 32;
+                    acc[q] = _mm512_fmadd_ps(w0, _mm512_loadu_ps(x), acc[q]);
+                    acc[q] = _mm512_fmadd_ps(w1, _mm512_loadu_ps(x + 16), acc[q]);
+                }
+        }
+        for (int q = 0; q < nb; ++q) out[j0 + q] = _mm512_reduce_add_ps(acc[q]);
+    }
+}
+
+using DotsMxFn = void (*)(const uint8_t*, const uint8_t*, size_t, const float*, size_t, int, float*);
+
+DotsMxFn pick_dots_mx() {
+    __builtin_cpu_init();
+    if (__builtin_cpu_supports("avx512f") && __builtin_cpu_supports("avx512bw")) return dots_mx_avx512;
+    return dots_mx_generic;
+}
+
 inline float silu(float u) { return u / (1.0f + std::exp(-u)); }
 
 }  // namespace
@@ -228,6 +289,8 @@ extern "C" spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, in
 
         int threads = n_threads > 0 ? n_threads : (int)std::max(1u, std::thread::hardware_concurrency());
         static const DotsFn dots = pick_dots();
+        static const DotsMxFn dots_mx = pick_dots_mx();
+        const bool mx = c.wfmt == SPICE_WFMT_MXFP4;
         Pool& pool = Pool::get();
 
         // x rows of the exact slots, widened to fp32 (one row per slot)
@@ -246,10 +309,20 @@ extern "C" spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, in
             const int e = experts[task / nb1], rb = task % nb1;
             const int n = count[e], base = first[e];
             const char* w13 = static_cast<const char*>(w13_host[e]);
+            // MXFP4 blob of [2I][d]: codes, then the scales
+            const uint8_t* el = reinterpret_cast<const uint8_t*>(w13);
+            const uint8_t* sc = el + (size_t)2 * I * (d / 2);
             std::vector<float> gv(n), uv(n);
             for (int i = rb * kRows1; i < std::min(I, (rb + 1) * kRows1); ++i) {
-                dots(w13 + (size_t)i * d * es, dt, d, &xs[(size_t)base * d], d, n, gv.data());
-                dots(w13 + (size_t)(I + i) * d * es, dt, d, &xs[(size_t)base * d], d, n, uv.data());
+                if (mx) {
+                    dots_mx(el + (size_t)i * (d / 2), sc + (size_t)i * (d / 32), d, &xs[(size_t)base * d], d, n,
+                            gv.data());
+                    dots_mx(el + (size_t)(I + i) * (d / 2), sc + (size_t)(I + i) * (d / 32), d,
+                            &xs[(size_t)base * d], d, n, uv.data());
+                } else {
+                    dots(w13 + (size_t)i * d * es, dt, d, &xs[(size_t)base * d], d, n, gv.data());
+                    dots(w13 + (size_t)(I + i) * d * es, dt, d, &xs[(size_t)base * d], d, n, uv.data());
+                }
                 for (int j = 0; j < n; ++j) h[(size_t)(base + j) * I + i] = silu(gv[j]) * uv[j];
             }
         });
@@ -257,9 +330,15 @@ extern "C" spice_status_t moe_exact_residual_host(const spice_moe_cfg_t* cfg, in
             const int e = experts[task / nb2], rb = task % nb2;
             const int n = count[e], base = first[e];
             const char* w2 = static_cast<const char*>(w2_host[e]);
+            const uint8_t* el = reinterpret_cast<const uint8_t*>(w2);  // MXFP4 blob of [d][I]
+            const uint8_t* sc = el + (size_t)d * (I / 2);
             std::vector<float> ov(n);
             for (int j = rb * kRows2; j < std::min(d, (rb + 1) * kRows2); ++j) {
-                dots(w2 + (size_t)j * I * es, dt, I, &h[(size_t)base * I], I, n, ov.data());
+                if (mx)
+                    dots_mx(el + (size_t)j * (I / 2), sc + (size_t)j * (I / 32), I, &h[(size_t)base * I], I, n,
+                            ov.data());
+                else
+                    dots(w2 + (size_t)j * I * es, dt, I, &h[(size_t)base * I], I, n, ov.data());
                 for (int q = 0; q < n; ++q) y[(size_t)(base + q) * d + j] = ov[q];
             }
         });

@@ -185,6 +185,8 @@ spice_status_t moe_lore_fit(const spice_moe_cfg_t* cfg, int32_t n, int32_t r, co
                             float* y_out, double* loss_out, void* ws, size_t ws_bytes, spice_stream_t stream) {
     try {
         spice_status_t st = spice::validate(cfg, n);
+        if (st == SPICE_OK && cfg->wfmt != SPICE_WFMT_DTYPE)
+            return spice::set_error(SPICE_ERR_UNSUPPORTED, "moe_lore_fit: needs SPICE_WFMT_DTYPE expert weights");
         if (st != SPICE_OK) return st;
         const spice_moe_cfg_t& c = *cfg;
         const int32_t d = c.d;

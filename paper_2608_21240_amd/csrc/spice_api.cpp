@@ -44,6 +44,12 @@ spice_status_t check_cfg(const spice_moe_cfg_t* c) {
     if (c->norm_topk != 0 && c->norm_topk != 1) return fail(SPICE_ERR_INVALID, "norm_topk must be 0 or 1");
     if (c->conf_mode < SPICE_CONF_INPUT || c->conf_mode > SPICE_CONF_GATE_RENORM)
         return fail(SPICE_ERR_INVALID, "conf_mode must be a SPICE_CONF_* value");
+    if (c->wfmt != SPICE_WFMT_DTYPE && c->wfmt != SPICE_WFMT_MXFP4)
+        return fail(SPICE_ERR_INVALID, "wfmt must be SPICE_WFMT_DTYPE or SPICE_WFMT_MXFP4");
+    if (c->wfmt == SPICE_WFMT_MXFP4 && c->dtype != SPICE_BF16)
+        return fail(SPICE_ERR_UNSUPPORTED, "MXFP4 expert weights need dtype SPICE_BF16");
+    if (c->wfmt == SPICE_WFMT_MXFP4 && (c->d % 32 || c->inter % 32))
+        return fail(SPICE_ERR_UNSUPPORTED, "MXFP4 expert weights need d and inter multiples of 32");
     const int al = c->dtype == SPICE_BF16 ? 8 : 4;
     if (c->d % al || c->inter % al || c->shared_inter % al || c->lore_rank % al)
         return fail(SPICE_ERR_UNSUPPORTED, "d, inter, shared_inter and lore_rank must be multiples of " +
@@ -273,13 +279,15 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
     a.lore_A = lore_A; a.lore_B = lore_B; a.y_slots = y_slots; a.y_shared = y_shared;
     a.h = wsb + L.h; a.hs = wsb + L.hs; a.u = reinterpret_cast<float*>(wsb + L.u);
     a.ctrl = reinterpret_cast<uint32_t*>(wsb);
+    a.wfmt = c.wfmt;
     if (w_shared_gate && (groups & spice::kDoShared) && c.shared_inter > 0) {
         float* sg = reinterpret_cast<float*>(wsb + L.sgate);
         hipError_t e = spice::launch_shared_gate(x, w_shared_gate, T, c.d, c.dtype, sg, stream);
         if (e != hipSuccess) return hip_fail(e, name);
         a.sgate = sg;
     }
-    hipError_t e = spice::launch_expert_ffn(a, stream);
+    hipError_t e = c.wfmt == SPICE_WFMT_MXFP4 ? spice::launch_expert_ffn_mx(a, stream)
+                                                : spice::launch_expert_ffn(a, stream);
     if (e != hipSuccess) return hip_fail(e, name);
     return SPICE_OK;
 }
@@ -334,6 +342,8 @@ spice_status_t moe_expert_ffn_fetched(const spice_moe_cfg_t* cfg, int32_t T, con
     if ((st = check_tokens(c, T)) != SPICE_OK) return st;
     if (n_slots < 1 || n_slots > c.n_experts)
         return fail(SPICE_ERR_INVALID, "moe_expert_ffn_fetched: n_slots must be in [1, n_experts]");
+    if (c.wfmt != SPICE_WFMT_DTYPE)
+        return fail(SPICE_ERR_UNSUPPORTED, "moe_expert_ffn_fetched: needs SPICE_WFMT_DTYPE expert weights");
     if (T == 0) return SPICE_OK;
     SPICE_REQUIRE(x, "x");
     SPICE_REQUIRE(perm, "perm");

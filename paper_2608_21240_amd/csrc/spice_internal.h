@@ -70,8 +70,19 @@ struct RouteArgs {
     int32_t* h_counts;
 };
 
+// Bytes of one routed expert's W13 [2I][d] and W2 [d][I] in the cfg's weight format.
+inline size_t expert_w13_bytes(const spice_moe_cfg_t& c) {
+    const size_t n = (size_t)2 * c.inter * c.d;
+    return c.wfmt == SPICE_WFMT_MXFP4 ? n / 2 + n / 32 : n * (c.dtype == SPICE_BF16 ? 2 : 4);
+}
+inline size_t expert_w2_bytes(const spice_moe_cfg_t& c) {
+    const size_t n = (size_t)c.inter * c.d;
+    return c.wfmt == SPICE_WFMT_MXFP4 ? n / 2 + n / 32 : n * (c.dtype == SPICE_BF16 ? 2 : 4);
+}
+
 struct FfnArgs {
     int32_t T, d, N, K, C, I, Is, r, dtype, groups;
+    int32_t wfmt;  // SPICE_WFMT_*: the pools hold MXFP4 blobs when SPICE_WFMT_MXFP4
     int32_t ldh, ldhs;  // row strides (elements) of h and hs
     const void* x;
     const int32_t* perm;
@@ -163,6 +174,8 @@ hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
+// The same launch with MXFP4 routed experts (expert_ffn_mx.hip).
+hipError_t launch_expert_ffn_mx(const FfnArgs& a, hipStream_t s);
 // sgate[t] = sigmoid(w_sg . x[t]) for T tokens (fp64 dot products), shared_gate.hip.
 hipError_t launch_shared_gate(const void* x, const void* w_sg, int32_t T, int32_t d, int32_t dtype, float* sgate,
                               hipStream_t s);

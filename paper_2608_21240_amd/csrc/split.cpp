@@ -36,6 +36,8 @@ spice_status_t moe_split_plan(const spice_moe_cfg_t* cfg, int32_t T, const int32
         if (!n_fetch) return err(SPICE_ERR_INVALID, "moe_split_plan: n_fetch is NULL");
         *n_fetch = 0;
         spice_status_t st = spice::validate(cfg, T);
+        if (st == SPICE_OK && cfg->wfmt != SPICE_WFMT_DTYPE)
+            return err(SPICE_ERR_UNSUPPORTED, "moe_split_plan: the fetched-expert split needs SPICE_WFMT_DTYPE weights");
         if (st != SPICE_OK) return st;
         if (!cost) return err(SPICE_ERR_INVALID, "moe_split_plan: cost is NULL");
         if (max_fetch < 0) return err(SPICE_ERR_INVALID, "moe_split_plan: max_fetch must be >= 0");
@@ -107,6 +109,8 @@ spice_status_t moe_fetch_experts(const spice_moe_cfg_t* cfg, int32_t n_fetch, co
                                  int32_t* fetch_expert_stage, spice_stream_t copy_stream) {
     try {
         spice_status_t st = spice::validate(cfg, 0);
+        if (st == SPICE_OK && cfg->wfmt != SPICE_WFMT_DTYPE)
+            return err(SPICE_ERR_UNSUPPORTED, "moe_fetch_experts: the fetched-expert split needs SPICE_WFMT_DTYPE weights");
         if (st != SPICE_OK) return st;
         const int N = cfg->n_experts;
         if (n_slots < 1 || n_slots > N) return err(SPICE_ERR_INVALID, "moe_fetch_experts: n_slots must be in [1, N]");

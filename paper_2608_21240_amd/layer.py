@@ -21,7 +21,7 @@ import numpy as np
 import torch
 
 from . import spice, synth
-from .workloads import DTYPE_BF16, Workload
+from .workloads import DTYPE_BF16, WFMT_MXFP4, Workload
 
 
 def torch_dtype(dtype: int) -> torch.dtype:
@@ -114,12 +114,19 @@ class DeviceLayer:
         slot = np.full(s.n_experts, -1, np.int32)
         host.prefetch(range(s.n_experts) if host_exact else host.resident,
                       range(s.n_experts) if s.lore_rank > 0 else ())
-        self.w13_pool = torch.empty((max(self.C, 1), 2 * s.inter, s.d), dtype=td, device=device)
-        self.w2_pool = torch.empty((max(self.C, 1), s.d, s.inter), dtype=td, device=device)
+        self.wfmt = host.wl.wfmt
+        if self.wfmt == WFMT_MXFP4:
+            # one MXFP4 byte blob per slot: [2I][d] and [d][I] (codes, then block scales)
+            b13, b2 = synth.mxfp4_bytes(2 * s.inter, s.d), synth.mxfp4_bytes(s.d, s.inter)
+            self.w13_pool = torch.empty((max(self.C, 1), b13), dtype=torch.uint8, device=device)
+            self.w2_pool = torch.empty((max(self.C, 1), b2), dtype=torch.uint8, device=device)
+        else:
+            self.w13_pool = torch.empty((max(self.C, 1), 2 * s.inter, s.d), dtype=td, device=device)
+            self.w2_pool = torch.empty((max(self.C, 1), s.d, s.inter), dtype=td, device=device)
         for i, e in enumerate(host.resident):
             w13, w2 = host.expert(e)
-            self.w13_pool[i].copy_(to_tensor(w13, dt))
-            self.w2_pool[i].copy_(to_tensor(w2, dt))
+            self.w13_pool[i].copy_(self._weights(w13))
+            self.w2_pool[i].copy_(self._weights(w2))
             slot[e] = i
         self.resident_slot = torch.from_numpy(slot).to(device)
         r = max(s.lore_rank, 1)
@@ -138,8 +145,15 @@ class DeviceLayer:
             for e in range(s.n_experts):
                 if slot[e] < 0:
                     w13, w2 = host.expert(e)
-                    self.host_w13[e] = to_tensor(w13, dt, pin=True)
-                    self.host_w2[e] = to_tensor(w2, dt, pin=True)
+                    self.host_w13[e] = self._weights(w13, pin=True)
+                    self.host_w2[e] = self._weights(w2, pin=True)
+
+    def _weights(self, a: np.ndarray, pin: bool = False) -> torch.Tensor:
+        """A routed expert's weight array (storage dtype, or an MXFP4 byte blob) as a tensor."""
+        if self.wfmt == WFMT_MXFP4:
+            t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8))
+            return t.pin_memory() if pin else t
+        return to_tensor(a, self.shape.dtype, pin=pin)
 
     def hbm_bytes(self) -> int:
         ts = [self.wg, self.w13s, self.w2s, self.w13_pool, self.w2_pool, self.lore_A, self.lore_B]
@@ -150,9 +164,9 @@ class LayerRun:
     """Buffers and streams for layer calls with up to T tokens."""
 
     def __init__(self, shape, T: int, n_slots: int, tau: float = 0.5, conf_mode: int = 0, norm_topk: int = 0,
-                 device: str = "cuda", keep_logits: bool = False, fetch_slots: int = 0):
+                 device: str = "cuda", keep_logits: bool = False, fetch_slots: int = 0, wfmt: int = 0):
         self.shape, self.T = shape, T
-        self.cfg = spice.make_cfg(shape, n_slots, tau, conf_mode, norm_topk)
+        self.cfg = spice.make_cfg(shape, n_slots, tau, conf_mode, norm_topk, wfmt)
         s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
         i32 = dict(dtype=torch.int32, device=device)
         f32 = dict(dtype=torch.float32, device=device)

@@ -19,6 +19,7 @@ SPICE_OK, SPICE_ERR_INVALID, SPICE_ERR_UNSUPPORTED, SPICE_ERR_HIP, SPICE_ERR_WOR
     0, -1, -2, -3, -4, -5)
 SPICE_F32, SPICE_BF16 = 0, 1
 SPICE_CONF_INPUT, SPICE_CONF_GATE, SPICE_CONF_GATE_RENORM = 0, 1, 2
+SPICE_WFMT_DTYPE, SPICE_WFMT_MXFP4 = 0, 2
 SPICE_CLASS_HIT, SPICE_CLASS_LORE, SPICE_CLASS_EXACT, SPICE_CLASS_EXACT_GPU = 0, 1, 2, 3
 SPICE_MAX_EXPERTS, SPICE_MAX_TOKENS, SPICE_MAX_LORE_RANK = 256, 65536, 256
 SPICE_WS_CONTROL_BYTES = 131072
@@ -47,7 +48,7 @@ class spice_moe_cfg_t(ctypes.Structure):
     _fields_ = [("d", ctypes.c_int32), ("n_experts", ctypes.c_int32), ("top_k", ctypes.c_int32),
                 ("inter", ctypes.c_int32), ("shared_inter", ctypes.c_int32), ("lore_rank", ctypes.c_int32),
                 ("n_slots", ctypes.c_int32), ("dtype", ctypes.c_int32), ("norm_topk", ctypes.c_int32),
-                ("conf_mode", ctypes.c_int32), ("tau", ctypes.c_float)]
+                ("conf_mode", ctypes.c_int32), ("tau", ctypes.c_float), ("wfmt", ctypes.c_int32)]
 
 
 class spice_split_cost_t(ctypes.Structure):
@@ -71,9 +72,9 @@ def host_out(x=None, topk_idx=None, topk_w=None, slot_class=None, class_counts=N
 
 
 def make_cfg(shape, n_slots: int, tau: float = 0.5, conf_mode: int = SPICE_CONF_INPUT,
-             norm_topk: int = 0) -> spice_moe_cfg_t:
+             norm_topk: int = 0, wfmt: int = 0) -> spice_moe_cfg_t:
     return spice_moe_cfg_t(shape.d, shape.n_experts, shape.top_k, shape.inter, shape.shared_inter,
-                           shape.lore_rank, n_slots, shape.dtype, norm_topk, conf_mode, tau)
+                           shape.lore_rank, n_slots, shape.dtype, norm_topk, conf_mode, tau, wfmt)
 
 
 _lib: Optional[ctypes.CDLL] = None

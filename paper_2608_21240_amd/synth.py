@@ -145,18 +145,17 @@ def quantize_mxfp4(a: np.ndarray) -> np.ndarray:
     assert K % 32 == 0
     blk = np.asarray(a, np.float64).reshape(rows, K // 32, 32)
     amax = np.abs(blk).max(axis=2)
-    with np.errstate(divide="ignore"):
-        ex = np.where(amax > 0, np.floor(np.log2(np.where(amax > 0, amax, 1.0))) - 2, 0).astype(np.int64)
+    ex = np.zeros(amax.shape, np.int64)
+    nz = amax > 0
+    ex[nz] = np.floor(np.log2(amax[nz])).astype(np.int64) - 2
     ex = np.clip(ex, -127, 127)
-    q = np.abs(blk) / np.ldexp(1.0, ex)[:, :, None]
-    dist = np.abs(q[..., None] - E2M1_MAGNITUDES)  # [rows][blocks][32][8]
-    best = dist.min(axis=-1, keepdims=True)
-    tie_ok = dist == best
-    # among equally near codes take the even one (the larger code when q saturates above 6)
-    even = (np.arange(8) % 2 == 0)
-    pick = np.where(tie_ok & even, np.arange(8), -1).max(axis=-1)
-    pick = np.where(pick >= 0, pick, np.argmax(tie_ok, axis=-1))
-    codes = (pick | np.where((blk < 0) & (pick > 0), 8, 0)).astype(np.uint8).reshape(rows, K)
+    q = (np.abs(blk) / np.ldexp(1.0, ex)[:, :, None]).reshape(-1)
+    mids = (E2M1_MAGNITUDES[1:] + E2M1_MAGNITUDES[:-1]) / 2  # decision points between codes
+    code = np.searchsorted(mids, q, side="left")  # q at a midpoint takes the lower code here
+    at_mid = (code < 7) & (q == mids[np.minimum(code, 6)])
+    code = np.where(at_mid & (code % 2 == 1), code + 1, code)  # ties to the even code
+    sign = (blk.reshape(-1) < 0) & (code > 0)
+    codes = (code | np.where(sign, 8, 0)).astype(np.uint8).reshape(rows, K)
     packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
     scales = (ex + 127).astype(np.uint8)
     return np.concatenate([packed.reshape(-1), scales.reshape(-1)])

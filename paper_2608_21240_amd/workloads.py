@@ -86,6 +86,9 @@ WORKLOADS = {
     "dsv2_decode_t1": Workload("dsv2_decode_t1", DSV2, tokens=1, resident=32, skew=False),
     "dsv2_decode_t8": Workload("dsv2_decode_t8", DSV2, tokens=8, resident=32, skew=False),
     "dsv2_decode_t32": Workload("dsv2_decode_t32", DSV2, tokens=32, resident=32, skew=False),
+    # the same layer with MXFP4 routed experts (quantised expert weights)
+    "dsv2_decode_mxfp4_t32": Workload("dsv2_decode_mxfp4_t32", DSV2, tokens=32, resident=32, skew=False,
+                                      wfmt=WFMT_MXFP4),
     "qwen2_decode_r16": Workload("qwen2_decode_r16", QWEN2, tokens=16, resident=16, skew=True),
     "qwen2_decode_r32": Workload("qwen2_decode_r32", QWEN2, tokens=16, resident=32, skew=True),
     "qwen2_decode_r48": Workload("qwen2_decode_r48", QWEN2, tokens=16, resident=48, skew=True),

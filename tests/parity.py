@@ -69,7 +69,8 @@ class Case:
         self.dev = dev if dev is not None else LY.DeviceLayer(self.host, n_slots=self.n_slots)
         self.run = run if run is not None else LY.LayerRun(s, self.T, self.dev.C, tau=self.wl.tau,
                                                             conf_mode=self.wl.conf_mode, norm_topk=self.wl.norm_topk,
-                                                            keep_logits=True, fetch_slots=fetch_slots)
+                                                            keep_logits=True, fetch_slots=fetch_slots,
+                                                            wfmt=self.wl.wfmt)
         R = self.run
         xd = LY.to_tensor(self.x, s.dtype, "cuda")
         conf = torch.from_numpy(np.ascontiguousarray(self.conf)).cuda()
@@ -96,7 +97,7 @@ class Case:
     # ------------------------------------------------------------------ oracle
     def run_oracle(self, tokens: Optional[Sequence[int]] = None):
         s, wl = self.shape, self.wl
-        cfg = orc.make_cfg(s, tau=wl.tau, conf_mode=wl.conf_mode, norm_topk=wl.norm_topk)
+        cfg = orc.make_cfg(s, tau=wl.tau, conf_mode=wl.conf_mode, norm_topk=wl.norm_topk, wfmt=wl.wfmt)
         self.cfg = cfg
         res = self.host.resident_mask()
         r = orc.route(cfg, self.x, self.host.wg, self.host.bias, res, self.conf)

@@ -14,8 +14,8 @@ def rel_err(out, ref):
     return num / den
 
 
-def setup(orc, shape, T, seed, exact_frac=0.6, resident_frac=0.3):
-    wl = W.Workload("t", shape, tokens=T, resident=0, skew=False, seed=seed)
+def setup(orc, shape, T, seed, exact_frac=0.6, resident_frac=0.3, wfmt=0):
+    wl = W.Workload("t", shape, tokens=T, resident=0, skew=False, seed=seed, wfmt=wfmt)
     r = np.random.default_rng(seed)
     N = shape.n_experts
     resident = np.zeros(N, np.int32)
@@ -23,7 +23,7 @@ def setup(orc, shape, T, seed, exact_frac=0.6, resident_frac=0.3):
     x = synth.gen_x(wl)
     wg = synth.gen_router(wl)
     conf = np.where(r.random((T, shape.top_k)) < exact_frac, 0.9, 0.1).astype(np.float32)
-    cfg = orc.make_cfg(shape)
+    cfg = orc.make_cfg(shape, wfmt=wfmt)
     rt = orc.route(cfg, x, wg, None, resident, conf)
     experts = sorted(set(rt["idx"][rt["cls"] == EXACT].tolist()))
     w13 = [None] * N
@@ -51,6 +51,39 @@ def test_exact_residual_matches_oracle(orc, shape, T, seed):
     assert (out[~has] == 0).all()
     tol = 1e-4  # fp32 arithmetic on exact inputs, for fp32 and bf16 storage alike
     assert rel_err(out[has], ref[has]).max() < tol
+
+
+@pytest.mark.parametrize("shape,T,seed", [
+    (W.small_shape(), 13, 4),
+    (W.MoEShape(2048, 64, 6, 1408, 2816, 32, W.DTYPE_BF16), 2, 6),
+])
+def test_exact_residual_mxfp4_matches_oracle(orc, shape, T, seed):
+    """MXFP4 expert weights: the host path decodes the same blobs the oracle reads."""
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, T, seed, wfmt=W.WFMT_MXFP4)
+    assert all(a is None or a.dtype == np.uint8 for a in w13)
+    ref = orc.exact_residual(cfg, x, rt["idx"], rt["g"], rt["cls"], w13, w2)
+    c = spice.make_cfg(shape, n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    gw = rt["g"].astype(np.float32)
+    outs = []
+    for nt in (1, 5):
+        out = np.full((T, shape.d), np.nan, np.float32)
+        spice.moe_exact_residual_host(c, T, x, rt["idx"], gw, rt["cls"], w13, w2, out, n_threads=nt)
+        outs.append(out)
+    assert np.array_equal(outs[0], outs[1])
+    has = (rt["cls"] == EXACT).any(axis=1)
+    assert has.any() and (outs[0][~has] == 0).all()
+    assert rel_err(outs[0][has], ref[has]).max() < 1e-4
+
+
+def test_mxfp4_config_rules():
+    bad = spice.make_cfg(W.small_shape(dtype=W.DTYPE_F32), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    assert spice.spice_workspace_bytes(bad, 4) == 0  # MXFP4 needs bf16 activations
+    odd = spice.make_cfg(W.MoEShape(200, 16, 4, 104, 168, 24, W.DTYPE_BF16), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    assert spice.spice_workspace_bytes(odd, 4) == 0  # d and inter multiples of 32
+    unknown = spice.make_cfg(W.small_shape(), n_slots=0, wfmt=1)
+    assert spice.spice_workspace_bytes(unknown, 4) == 0
+    ok = spice.make_cfg(W.small_shape(), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    assert spice.spice_workspace_bytes(ok, 4) > 0
 
 
 def test_result_is_independent_of_thread_count(orc):
