@@ -100,10 +100,12 @@ typedef struct {
  *   consecutive elements of a row; element value = 2^(scale - 127) * e2m1(code).  A W13 blob
  *   holds [2I][d] (2I*d*17/32 bytes), a W2 blob [d][I] (d*I*17/32 bytes); a pool slot is one
  *   such blob.  Needs dtype SPICE_BF16 (activations, router, shared block and LoRE factors
- *   stay bf16) and d, inter multiples of 32.  The fetched-expert split (moe_split_plan,
+ *   stay bf16), d and inter multiples of 32 and at most SPICE_MXFP4_MAX_K, and blobs below
+ *   2 GiB.  The fetched-expert split (moe_split_plan,
  *   moe_fetch_experts, moe_expert_ffn_fetched) and moe_lore_fit return UNSUPPORTED for it;
  *   at any T the expert FFN runs on the streaming kernels, not the prefill GEMMs. */
 enum { SPICE_WFMT_DTYPE = 0, SPICE_WFMT_MXFP4 = 2 };
+#define SPICE_MXFP4_MAX_K 4096
 
 /* Size alignment required: d, inter and shared_inter multiples of 8 (bf16) or 4 (fp32);
  * lore_rank a multiple of 8 (bf16) or 4 (fp32). */

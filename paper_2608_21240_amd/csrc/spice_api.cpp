@@ -50,6 +50,8 @@ spice_status_t check_cfg(const spice_moe_cfg_t* c) {
         return fail(SPICE_ERR_UNSUPPORTED, "MXFP4 expert weights need dtype SPICE_BF16");
     if (c->wfmt == SPICE_WFMT_MXFP4 && (c->d % 32 || c->inter % 32))
         return fail(SPICE_ERR_UNSUPPORTED, "MXFP4 expert weights need d and inter multiples of 32");
+    if (c->wfmt == SPICE_WFMT_MXFP4 && (c->d > SPICE_MXFP4_MAX_K || c->inter > SPICE_MXFP4_MAX_K))
+        return fail(SPICE_ERR_UNSUPPORTED, "MXFP4 expert weights need d and inter at most SPICE_MXFP4_MAX_K");
     const int al = c->dtype == SPICE_BF16 ? 8 : 4;
     if (c->d % al || c->inter % al || c->shared_inter % al || c->lore_rank % al)
         return fail(SPICE_ERR_UNSUPPORTED, "d, inter, shared_inter and lore_rank must be multiples of " +
@@ -263,6 +265,9 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
         SPICE_REQUIRE(lore_B, "lore_B");
     }
     if ((st = check_ws(c, T, ws, ws_bytes)) != SPICE_OK) return st;
+    if (c.wfmt == SPICE_WFMT_MXFP4 && ((size_t)T * c.top_k * ((size_t)c.inter + spice::kHPad) * 2 >= (1ull << 31) ||
+                                       (size_t)T * c.d * 2 >= (1ull << 31)))
+        return fail(SPICE_ERR_UNSUPPORTED, std::string(name) + ": MXFP4 experts need x and H below 2 GiB");
     const size_t ysz = (size_t)T * c.top_k * c.d * sizeof(float);
     if (overlaps(y_slots, ysz, x, (size_t)T * c.d * elem_size(c)) ||
         overlaps(y_shared, (size_t)T * c.d * sizeof(float), x, (size_t)T * c.d * elem_size(c)) ||

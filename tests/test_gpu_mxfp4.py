@@ -45,6 +45,22 @@ def test_mxfp4_layers(shape, T, R, fused):
     assert (counts > 0).all(), counts
 
 
+# the widest contractions MXFP4 takes (SPICE_MXFP4_MAX_K): 128 scales per row in the up
+# pass (d = 4096) and in the down pass (inter = 4096)
+MX_WIDE_D = W.MoEShape(d=4096, n_experts=8, top_k=2, inter=1024, shared_inter=256, lore_rank=16, dtype=W.DTYPE_BF16)
+MX_WIDE_I = W.MoEShape(d=1024, n_experts=8, top_k=2, inter=4096, shared_inter=256, lore_rank=16, dtype=W.DTYPE_BF16)
+
+
+@pytest.mark.parametrize("shape", [MX_WIDE_D, MX_WIDE_I], ids=["d4096", "inter4096"])
+def test_mxfp4_widest_rows(shape):
+    say(f"mxfp4 d={shape.d} I={shape.inter} T=20")
+    c = Case(mx(shape, 20, 4))
+    c.run_gpu()
+    c.run_oracle(tokens=[0, 7, 19])
+    c.check_routing()
+    c.check_outputs()
+
+
 def test_mxfp4_gated_shared_block():
     c = Case(mx(MX_B, 19, 6, shared_gate=True))
     c.run_gpu()

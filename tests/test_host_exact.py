@@ -82,6 +82,11 @@ def test_mxfp4_config_rules():
     assert spice.spice_workspace_bytes(odd, 4) == 0  # d and inter multiples of 32
     unknown = spice.make_cfg(W.small_shape(), n_slots=0, wfmt=1)
     assert spice.spice_workspace_bytes(unknown, 4) == 0
+    wide = spice.make_cfg(W.MoEShape(4128, 16, 4, 128, 128, 8, W.DTYPE_BF16), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    assert spice.spice_workspace_bytes(wide, 4) == 0  # d above the MXFP4 limit (4096)
+    assert "SPICE_MXFP4_MAX_K" in spice.last_error()
+    edge = spice.make_cfg(W.MoEShape(4096, 16, 4, 4096, 128, 8, W.DTYPE_BF16), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    assert spice.spice_workspace_bytes(edge, 4) > 0
     ok = spice.make_cfg(W.small_shape(), n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
     assert spice.spice_workspace_bytes(ok, 4) > 0
 
