@@ -38,16 +38,28 @@ METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shap
 # HBM traffic of one grouped-FFN call (up + down kernels) at the headline batch, from
 # two rocprofv3 --pmc passes over this script (FETCH_SIZE, then WRITE_SIZE; KiB per
 # dispatch) scaled by what the counters read for a plain 1 GiB device copy
-# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  Reported only while the kernel sources (the
-# two files hashed together) are the ones the counters were taken on.
-TRAFFIC_RECORD = {
-    "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
-    "source_sha256_16": "a34166ed9f8959c3",
-    "fetch_kib_per_call": 189122.92 + 96783.86,
-    "write_kib_per_call": 462.50 + 1451.88,
-    "fetch_factor": 2.0,
-    "write_factor": 1.0,
-    "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
+# (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  One record per expert weight format; each is
+# reported only while the kernel sources (the files hashed together) are the ones the
+# counters were taken on.
+TRAFFIC_RECORDS = {
+    "bf16": {
+        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
+        "source_sha256_16": "a34166ed9f8959c3",
+        "fetch_kib_per_call": 189122.92 + 96783.86,
+        "write_kib_per_call": 462.50 + 1451.88,
+        "fetch_factor": 2.0,
+        "write_factor": 1.0,
+        "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
+    },
+    "mxfp4": {
+        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn_mx.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
+        "source_sha256_16": "b9ad1696bd7c26ef",
+        "fetch_kib_per_call": 60295.41 + 32806.65,
+        "write_kib_per_call": 462.62 + 1451.87,
+        "fetch_factor": 2.0,
+        "write_factor": 1.0,
+        "profile": "profiles/ffn_dsv2_decode_T32_mxfp4.md",
+    },
 }
 
 
@@ -82,18 +94,20 @@ def parse():
     return p.parse_args()
 
 
-def recorded_traffic():
-    """HBM bytes per grouped-FFN call from the counter record, or None if the kernel changed."""
+def recorded_traffic(weights: str = "bf16"):
+    """HBM bytes per grouped-FFN call from the counter record of this weight format, or None
+    if there is none or the kernel changed since it was taken."""
     import hashlib
 
-    h = hashlib.sha256()
-    for rel in TRAFFIC_RECORD["kernel_sources"]:
-        h.update(open(os.path.join(ROOT, rel), "rb").read())
-    sha = h.hexdigest()[:16]
-    if sha != TRAFFIC_RECORD["source_sha256_16"]:
+    rec = TRAFFIC_RECORDS.get(weights)
+    if rec is None:
         return None
-    return int(1024 * (TRAFFIC_RECORD["fetch_kib_per_call"] * TRAFFIC_RECORD["fetch_factor"]
-                       + TRAFFIC_RECORD["write_kib_per_call"] * TRAFFIC_RECORD["write_factor"]))
+    h = hashlib.sha256()
+    for rel in rec["kernel_sources"]:
+        h.update(open(os.path.join(ROOT, rel), "rb").read())
+    if h.hexdigest()[:16] != rec["source_sha256_16"]:
+        return None
+    return int(1024 * (rec["fetch_kib_per_call"] * rec["fetch_factor"] + rec["write_kib_per_call"] * rec["write_factor"]))
 
 
 def expert_bytes(wl) -> int:
@@ -257,7 +271,7 @@ def main():
                      " (moe_expert_ffn_grouped with LoRE fused)",
                      "achieved": round(head["ffn_launch_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(head["ffn_launch_GBps"] / HBM_PEAK_GBS, 4),
-                     "traffic": None if mx else recorded_traffic(),
+                     "traffic": recorded_traffic(args.weights),
                      "bytes_per_launch": int(head["ffn_launch_bytes"]), "avg_launch_us": round(head["ffn_launch_us"], 2),
                      "in_step_us": round(head["ffn_us"], 2)},
         "gpu_path": {"tokens_per_s": round(head["gpu_tokens_per_s"], 1), "ms_per_step": round(head["gpu_ms_per_step"], 4),

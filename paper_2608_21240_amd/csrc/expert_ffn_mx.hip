@@ -41,9 +41,10 @@ __device__ __forceinline__ size_t expert_w2_bytes_dev(const FfnArgs& a) {
     return n / 2 + n / 32;
 }
 
-// E8M0 block scale -> fp32 2^(s - 127) (s = 255 is NaN); the conversion applies it exactly.
+// E8M0 block scale -> fp32 2^(s - 127): the exponent field for s >= 1, the subnormal
+// 2^-127 for s = 0, NaN for s = 255; the conversion applies it exactly.
 __device__ __forceinline__ float e8m0(uint32_t s) {
-    return s == 255u ? __uint_as_float(0x7FC00000u) : __uint_as_float(s << 23);
+    return s == 255u ? __uint_as_float(0x7FC00000u) : s == 0u ? __uint_as_float(0x00400000u) : __uint_as_float(s << 23);
 }
 
 // 32 E2M1 codes (16 bytes) times the block scale -> 32 bf16 as four MFMA A operands:
