@@ -151,25 +151,59 @@ __attribute__((target("avx512f,avx512bw,avx512vl,fma"))) inline __m512 load16_av
     return _mm512_loadu_ps(static_cast<const float*>(w) + i);
 }
 
-// Tokens in blocks of 8: each weight chunk is converted once and used 8 times.
+// NT tokens at once, NA independent accumulators per token: each 16-element weight chunk
+// is converted once and used NT times, and NA chains hide the FMA latency when NT is small.
+template <int NT, int NA>
+__attribute__((target("avx512f,avx512bw,avx512vl,fma"))) inline void dots_block_avx512(const void* w, int dtype,
+                                                                                         size_t len, const float* xs,
+                                                                                         size_t ld, float* out) {
+    __m512 acc[NT][NA];
+#pragma GCC unroll 8
+    for (int q = 0; q < NT; ++q)
+#pragma GCC unroll 4
+        for (int c = 0; c < NA; ++c) acc[q][c] = _mm512_setzero_ps();
+    size_t i = 0;
+    for (; i + 16 * NA <= len; i += 16 * NA) {
+#pragma GCC unroll 4
+        for (int c = 0; c < NA; ++c) {
+            const __m512 wv = load16_avx512(w, dtype, i + 16 * c);
+#pragma GCC unroll 8
+            for (int q = 0; q < NT; ++q)
+                acc[q][c] = _mm512_fmadd_ps(wv, _mm512_loadu_ps(xs + (size_t)q * ld + i + 16 * c), acc[q][c]);
+        }
+    }
+    for (; i + 16 <= len; i += 16) {
+        const __m512 wv = load16_avx512(w, dtype, i);
+#pragma GCC unroll 8
+        for (int q = 0; q < NT; ++q) acc[q][0] = _mm512_fmadd_ps(wv, _mm512_loadu_ps(xs + (size_t)q * ld + i), acc[q][0]);
+    }
+#pragma GCC unroll 8
+    for (int q = 0; q < NT; ++q) {
+        __m512 t = acc[q][0];
+#pragma GCC unroll 4
+        for (int c = 1; c < NA; ++c) t = _mm512_add_ps(t, acc[q][c]);
+        float sum = _mm512_reduce_add_ps(t);
+        for (size_t k = i; k < len; ++k) sum += load_w(w, dtype, k) * xs[(size_t)q * ld + k];
+        out[q] = sum;
+    }
+}
+
+// Tokens in blocks of at most 8; fewer tokens take more accumulators per token.
 __attribute__((target("avx512f,avx512bw,avx512vl,fma"))) void dots_avx512(const void* w, int dtype, size_t len,
                                                                             const float* xs, size_t ld, int n,
                                                                             float* out) {
-    const size_t main = len & ~(size_t)15;
-    for (int j0 = 0; j0 < n; j0 += 8) {
-        const int nb = std::min(8, n - j0);
-        __m512 acc[8];
-        for (int q = 0; q < 8; ++q) acc[q] = _mm512_setzero_ps();
-        for (size_t i = 0; i < main; i += 16) {
-            const __m512 wv = load16_avx512(w, dtype, i);
-            for (int q = 0; q < 8; ++q)
-                if (q < nb) acc[q] = _mm512_fmadd_ps(wv, _mm512_loadu_ps(xs + (size_t)(j0 + q) * ld + i), acc[q]);
-        }
-        for (int q = 0; q < nb; ++q) {
-            float s = _mm512_reduce_add_ps(acc[q]);
-            for (size_t i = main; i < len; ++i) s += load_w(w, dtype, i) * xs[(size_t)(j0 + q) * ld + i];
-            out[j0 + q] = s;
-        }
+    int j = 0;
+    for (; j + 8 <= n; j += 8) dots_block_avx512<8, 1>(w, dtype, len, xs + (size_t)j * ld, ld, out + j);
+    const float* x = xs + (size_t)j * ld;
+    switch (n - j) {
+        case 1: dots_block_avx512<1, 4>(w, dtype, len, x, ld, out + j); break;
+        case 2: dots_block_avx512<2, 4>(w, dtype, len, x, ld, out + j); break;
+        case 3: dots_block_avx512<3, 2>(w, dtype, len, x, ld, out + j); break;
+        case 4: dots_block_avx512<4, 2>(w, dtype, len, x, ld, out + j); break;
+        case 5: dots_block_avx512<5, 1>(w, dtype, len, x, ld, out + j); break;
+        case 6: dots_block_avx512<6, 1>(w, dtype, len, x, ld, out + j); break;
+        case 7: dots_block_avx512<7, 1>(w, dtype, len, x, ld, out + j); break;
+        default: break;
     }
 }
 
@@ -186,7 +220,14 @@ DotsFn pick_dots() {
 const float kE2M1[16] = {0.0f, 0.5f, 1.0f, 1.5f, 2.0f, 3.0f, 4.0f, 6.0f,
                          -0.0f, -0.5f, -1.0f, -1.5f, -2.0f, -3.0f, -4.0f, -6.0f};
 
-inline float e8m0(uint8_t s) { return s == 255 ? std::nanf("") : std::ldexp(1.0f, (int)s - 127); }
+// E8M0 scale 2^(s - 127) from its bits: the exponent field for s >= 1, the subnormal 2^-127
+// for s = 0, NaN for s = 255.
+inline float e8m0(uint8_t s) {
+    const uint32_t bits = s == 255 ? 0x7FC00000u : s == 0 ? 0x00400000u : (uint32_t)s << 23;
+    float f;
+    std::memcpy(&f, &bits, 4);
+    return f;
+}
 
 void dots_mx_generic(const uint8_t* el, const uint8_t* sc, size_t len, const float* xs, size_t ld, int n,
                      float* out) {
@@ -205,31 +246,61 @@ void dots_mx_generic(const uint8_t* el, const uint8_t* sc, size_t len, const flo
     }
 }
 
-// Each block is decoded once (table permute of the 32 codes, times the scale) and used for
-// up to 8 tokens.
+// NT tokens at once: each 32-element block is decoded once (table permute of the codes,
+// with the table times the scale) and used NT times; two blocks per step and one
+// accumulator per half block give 4 independent chains per token.
+template <int NT>
+__attribute__((target("avx512f,avx512bw,avx512vl,fma"))) inline void dots_mx_step(const uint8_t* el, const uint8_t* sc,
+                                                                                    size_t blk, const float* xs,
+                                                                                    size_t ld, __m512 (&acc)[NT][4],
+                                                                                    int c0) {
+    const __m512 lut = _mm512_loadu_ps(kE2M1);
+    const __m128i low4 = _mm_set1_epi8(0x0F);
+    const __m128i bytes = _mm_loadu_si128(reinterpret_cast<const __m128i*>(el + blk * 16));
+    const __m128i lo = _mm_and_si128(bytes, low4), hi = _mm_and_si128(_mm_srli_epi16(bytes, 4), low4);
+    const __m512 ls = _mm512_mul_ps(lut, _mm512_set1_ps(e8m0(sc[blk])));
+    const __m512 w0 = _mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpacklo_epi8(lo, hi)), ls);
+    const __m512 w1 = _mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpackhi_epi8(lo, hi)), ls);
+#pragma GCC unroll 8
+    for (int q = 0; q < NT; ++q) {
+        const float* x = xs + (size_t)q * ld + blk * 32;
+        acc[q][c0] = _mm512_fmadd_ps(w0, _mm512_loadu_ps(x), acc[q][c0]);
+        acc[q][c0 + 1] = _mm512_fmadd_ps(w1, _mm512_loadu_ps(x + 16), acc[q][c0 + 1]);
+    }
+}
+
+template <int NT>
+__attribute__((target("avx512f,avx512bw,avx512vl,fma"))) inline void dots_mx_block_avx512(
+    const uint8_t* el, const uint8_t* sc, size_t len, const float* xs, size_t ld, float* out) {
+    __m512 acc[NT][4];
+#pragma GCC unroll 8
+    for (int q = 0; q < NT; ++q)
+#pragma GCC unroll 4
+        for (int c = 0; c < 4; ++c) acc[q][c] = _mm512_setzero_ps();
+    const size_t nblk = len / 32;
+    size_t b = 0;
+    for (; b + 2 <= nblk; b += 2) {
+        dots_mx_step<NT>(el, sc, b, xs, ld, acc, 0);
+        dots_mx_step<NT>(el, sc, b + 1, xs, ld, acc, 2);
+    }
+    if (b < nblk) dots_mx_step<NT>(el, sc, b, xs, ld, acc, 0);
+#pragma GCC unroll 8
+    for (int q = 0; q < NT; ++q)
+        out[q] = _mm512_reduce_add_ps(
+            _mm512_add_ps(_mm512_add_ps(acc[q][0], acc[q][1]), _mm512_add_ps(acc[q][2], acc[q][3])));
+}
+
 __attribute__((target("avx512f,avx512bw,avx512vl,fma"))) void dots_mx_avx512(const uint8_t* el, const uint8_t* sc,
                                                                                size_t len, const float* xs,
                                                                                size_t ld, int n, float* out) {
-    const __m512 lut = _mm512_loadu_ps(kE2M1);
-    const __m128i low4 = _mm_set1_epi8(0x0F);
-    for (int j0 = 0; j0 < n; j0 += 8) {
-        const int nb = std::min(8, n - j0);
-        __m512 acc[8];
-        for (int q = 0; q < 8; ++q) acc[q] = _mm512_setzero_ps();
-        for (size_t b = 0; b < len / 32; ++b) {
-            const __m128i bytes = _mm_loadu_si128(reinterpret_cast<const __m128i*>(el + b * 16));
-            const __m128i lo = _mm_and_si128(bytes, low4), hi = _mm_and_si128(_mm_srli_epi16(bytes, 4), low4);
-            const __m512 s = _mm512_set1_ps(e8m0(sc[b]));
-            const __m512 w0 = _mm512_mul_ps(_mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpacklo_epi8(lo, hi)), lut), s);
-            const __m512 w1 = _mm512_mul_ps(_mm512_permutexvar_ps(_mm512_cvtepu8_epi32(_mm_unpackhi_epi8(lo, hi)), lut), s);
-            for (int q = 0; q < 8; ++q)
-                if (q < nb) {
-                    const float* x = xs + (size_t)(j0 + q) * ld + b * 32;
-                    acc[q] = _mm512_fmadd_ps(w0, _mm512_loadu_ps(x), acc[q]);
-                    acc[q] = _mm512_fmadd_ps(w1, _mm512_loadu_ps(x + 16), acc[q]);
-                }
-        }
-        for (int q = 0; q < nb; ++q) out[j0 + q] = _mm512_reduce_add_ps(acc[q]);
+    int j = 0;
+    for (; j + 4 <= n; j += 4) dots_mx_block_avx512<4>(el, sc, len, xs + (size_t)j * ld, ld, out + j);
+    const float* x = xs + (size_t)j * ld;
+    switch (n - j) {
+        case 1: dots_mx_block_avx512<1>(el, sc, len, x, ld, out + j); break;
+        case 2: dots_mx_block_avx512<2>(el, sc, len, x, ld, out + j); break;
+        case 3: dots_mx_block_avx512<3>(el, sc, len, x, ld, out + j); break;
+        default: break;
     }
 }
 

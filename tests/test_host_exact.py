@@ -148,3 +148,33 @@ def test_exact_gpu_slots_are_left_to_the_gpu(orc):
     ref = orc.exact_residual(orc.make_cfg(shape), x, rt["idx"], rt["g"], only, w13, w2)
     err = np.abs(out - ref).max() / max(np.abs(ref).max(), 1e-30)
     assert err < 1e-4 if shape.dtype == 0 else err < 2e-2
+
+
+def test_exact_residual_mxfp4_scale_bytes(orc):
+    """E8M0 edge bytes on the host path: 0 is 2^-127 (tiny, not zero, as in the oracle), 1 is
+    2^-126, 255 is NaN, 100 an ordinary small scale; the oracle's decode of the same blobs
+    is the reference.  (Large scales overflow fp32 in SwiGLU, as they would in any fp32
+    evaluation, so they are not a parity case.)"""
+    shape = W.small_shape()
+    wl, cfg, x, rt, w13, w2 = setup(orc, shape, 7, 8, wfmt=W.WFMT_MXFP4)
+    c = spice.make_cfg(shape, n_slots=0, wfmt=spice.SPICE_WFMT_MXFP4)
+    gw = rt["g"].astype(np.float32)
+    has = (rt["cls"] == EXACT).any(axis=1)
+    assert has.any()
+    n13 = 2 * shape.inter * shape.d // 2
+    for byte in (0, 1, 100, 255):
+        a13 = [None if b is None else b.copy() for b in w13]
+        for b in a13:
+            if b is not None:
+                b[n13:] = byte  # every W1/W3 block scale
+        out = np.full((7, shape.d), np.nan, np.float32)
+        spice.moe_exact_residual_host(c, 7, x, rt["idx"], gw, rt["cls"], a13, w2, out, n_threads=3)
+        ref = orc.exact_residual(cfg, x, rt["idx"], rt["g"], rt["cls"], a13, w2)
+        if byte == 255:
+            assert np.isnan(out[has]).all() and np.isnan(ref[has]).all()
+            continue
+        assert np.isfinite(out[has]).all() and np.isfinite(ref[has]).all()
+        if byte <= 1:  # SiLU(g) u with g, u ~ 1e-38: below 1e-70, zero in fp32
+            assert np.abs(ref[has]).max() < 1e-60 and (np.abs(out[has]) < 1e-30).all()
+        else:
+            assert rel_err(out[has], ref[has]).max() < 1e-4
