@@ -206,7 +206,7 @@ def main():
                 i = w % args.instances
                 run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, split=split)
             torch.cuda.synchronize()
-        fetched = []
+        fetched, host_t, host_e = [], [], []
 
         names = ("start", "routed", "ffn0", "experts", "resid", "end")
         evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
@@ -219,6 +219,8 @@ def main():
             run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, events=evs[k], split=split)
             host_s += time.perf_counter() - h0
             fetched.append(len(run.last_fetch))
+            host_t.append(run.last_host_s)
+            host_e.append(run.last_host_experts)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
 
@@ -241,6 +243,8 @@ def main():
             ffn_GBps=float(ffn_bytes.sum() / (ffn_ms.sum() * 1e-3) / 1e9),
             ffn_bytes_per_launch=float(ffn_bytes.mean()),
             fetched_experts_per_step=float(np.mean(fetched)),
+            host_exact_ms=float(np.mean(host_t) * 1e3), host_exact_experts=float(np.mean(host_e)),
+            host_exact_GBps=float(np.sum(host_e) * expert_bytes(wl) / max(np.sum(host_t), 1e-12) / 1e9),
             classes=per_inst[0]["slots"], hit_experts=[p["hit_experts"] for p in per_inst],
             lore_experts=[p["lore_experts"] for p in per_inst], exact_experts=[p["exact_experts"] for p in per_inst],
         )
@@ -278,6 +282,9 @@ def main():
                      "GBps": round(head["gpu_GBps"], 1), "frac_hbm_peak": round(head["gpu_GBps"] / HBM_PEAK_GBS, 4),
                      "route_us": round(head["route_us"], 2), "ffn_us": round(head["ffn_us"], 2),
                      "combine_us": round(head["combine_us"], 2)},
+        "host_path": {"exact_ms": round(head["host_exact_ms"], 3), "experts_per_step": round(head["host_exact_experts"], 2),
+                      "GBps": round(head["host_exact_GBps"], 1),
+                      "note": "exact-miss residual on the host CPU (Eq. 12 M_cpu): bound by host DRAM reads"},
         "by_batch": {str(T): {k: (round(v, 3) if isinstance(v, float) else v) for k, v in r.items()}
                      for T, r in results.items()},
         "exact_split": {"mode": args.split, "fetch_slots": args.fetch_slots if args.split == "auto" else 0,

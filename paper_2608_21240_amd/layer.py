@@ -15,9 +15,11 @@ Every arithmetic step runs inside libspice_moe (HIP kernels or its host path).
 from __future__ import annotations
 
 import os
+import time
 from typing import Dict, List, Optional, Sequence
 
 import numpy as np
+
 import torch
 
 from . import spice, synth
@@ -207,6 +209,8 @@ class LayerRun:
             self.e_pool_free = torch.cuda.Event()
             self.e_pool_free.record(torch.cuda.current_stream())
         self.last_fetch: List[int] = []
+        self.last_host_s = 0.0  # wall time of the last host residual call
+        self.last_host_experts = 0  # distinct experts it read
 
     # -- the steps, each one C-ABI call ------------------------------------------------
     def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
@@ -265,8 +269,13 @@ class LayerRun:
                                              self.fetch_expert, self.w13_fetch, self.w2_fetch, self.fetch_slots,
                                              self.y_slots, self.ws, self.ws_bytes)
                 self.e_pool_free.record(cur)
+        # the slots left EXACT after the plan are the host's share (timed for the benchmark)
+        cls = self.cls_host[:T].numpy()
+        self.last_host_experts = len(set(self.idx_host[:T].numpy()[cls == spice.SPICE_CLASS_EXACT].tolist()))
+        t0 = time.perf_counter()
         spice.moe_exact_residual_host(self.cfg, T, self.x_host, self.idx_host, self.w_host, self.cls_host,
                                       L.host_w13, L.host_w2, self.resid, n_threads)
+        self.last_host_s = time.perf_counter() - t0
 
     def forward(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
                 exact: bool = True, n_threads: int = 0, events: Optional[Dict[str, torch.cuda.Event]] = None,
