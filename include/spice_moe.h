@@ -122,12 +122,13 @@ spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags,
                                      spice_stream_t stream);
 
 /*
- * Host copies written by moe_route_bucket for the exact CPU path (Sec. 4.3: the hidden
- * state and the routing decision of the exact misses go to the CPU).  Each pointer is
- * pinned host memory that the GPU can write (hipHostMalloc, torch's pin_memory), or NULL
- * to skip that copy; pageable memory is rejected.  The route kernel writes them over
- * PCIe; they are complete once the stream has passed the call (an event recorded after
- * it has completed).
+ * Host copies written by moe_route_bucket (and moe_layer_gpu) for the exact CPU path
+ * (Sec. 4.3: the hidden state and the routing decision of the exact misses go to the CPU).
+ * Each pointer is pinned host memory that the GPU can write (hipHostMalloc, torch's
+ * pin_memory), or NULL to skip that copy; pageable memory is rejected.  A kernel writes
+ * them over PCIe; they are complete once the stream has passed the call, or, earlier,
+ * once *ready holds ready_value: the kernel stores ready_value after every copy has
+ * landed (spice_wait_ready waits for it on the host).  Use a new ready_value per call.
  */
 typedef struct {
     void* x;               /* [T][d] dtype: the activations */
@@ -135,7 +136,14 @@ typedef struct {
     float* topk_w;         /* [T][K] */
     uint8_t* slot_class;   /* [T][K] */
     int32_t* class_counts; /* [3]: slots per class (HIT, LORE, EXACT) */
+    uint32_t* ready;       /* [1] or NULL: receives ready_value after the copies above */
+    uint32_t ready_value;
 } spice_host_out_t;
+
+/* Wait on the host until *ready == value (a pinned word a kernel writes, e.g.
+ * spice_host_out_t.ready).  Returns SPICE_ERR_HIP with a message if timeout_us passes
+ * first (timeout_us <= 0: wait up to 10 s), INVALID for a NULL pointer. */
+spice_status_t spice_wait_ready(const volatile uint32_t* ready, uint32_t value, int64_t timeout_us);
 
 /*
  * Steps 1-2: router logits z = x Wg^T (+ bias), softmax over all N, top-K by logit
@@ -157,6 +165,10 @@ typedef struct {
  *   perm          device [T*K] int32 out: perm[pos] = slot id
  *   inv_perm      device [T*K] int32 out: inv_perm[slot] = pos
  *   host_out      host copies for the CPU path (see spice_host_out_t), or NULL
+ * The workspace also receives the device work lists of the buckets (per class, the
+ * non-empty buckets in ascending expert order with start and size), which the fused
+ * layer path reads.  T <= 256 runs one block per token and one bucketing block; larger
+ * T computes the logits as fp64 MFMA tiles.
  */
 spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
                                 const void* w_gate, const float* logit_bias,
@@ -236,6 +248,35 @@ spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* t
                            const uint8_t* slot_class, const int32_t* inv_perm,
                            const float* y_slots, const float* y_shared, const float* resid,
                            void* out, spice_stream_t stream);
+
+/*
+ * Steps 1-4 (and 6 when out != NULL) of one layer call, enqueued on `stream` as one unit:
+ * routing and bucketing (as moe_route_bucket), the grouped FFN of the HIT slots and the
+ * shared block with the LoRE corrections fused (as moe_expert_ffn_grouped, or
+ * moe_expert_ffn_grouped_gated when w_shared_gate != NULL), then, if out != NULL, the
+ * combine with `resid` (as moe_combine).  Every output is the one those calls define.
+ * The work that does not depend on routing is not ordered after it (Sec. 4.2: the shared
+ * block S is always resident): for dtype experts with T <= 256 and T*K <= 1024 the call is
+ * three launches in which routing runs beside the shared block's up projection, the
+ * shared block's down projection beside the routed up projections, and each routed tile
+ * finds its bucket from the routing itself; otherwise the separate launches of those calls.
+ * For the CPU path of Sec. 4.3, pass host_out (its ready word is stored as soon as the
+ * copies have landed, before the FFN ends) and out = NULL, run moe_exact_residual_host on
+ * the copies, then moe_combine.
+ *   Arguments: as in moe_route_bucket, moe_expert_ffn_grouped(_gated) and moe_combine;
+ *   lore_A / lore_B NULL: no LoRE rows (call lore_surrogate_apply separately);
+ *   resid, out as in moe_combine (out NULL: no combine; resid is then ignored).
+ * Errors: those of the calls it stands for.
+ */
+spice_status_t moe_layer_gpu(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
+                             const float* logit_bias, const int32_t* resident_slot, const float* conf,
+                             const void* w13_pool, const void* w2_pool, const void* w13_shared,
+                             const void* w2_shared, const void* w_shared_gate, const void* lore_A,
+                             const void* lore_B, double* logits, int32_t* topk_idx, float* topk_w,
+                             uint8_t* slot_class, int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                             float* y_slots, float* y_shared, const spice_host_out_t* host_out,
+                             const float* resid, void* out, void* ws, size_t ws_bytes,
+                             spice_stream_t stream);
 
 /*
  * Step 5, host side: resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t) computed on the

@@ -30,7 +30,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     if (tile.kind != kKindShared &&
         !find_group(a, tile.kind == kKindHit ? SPICE_CLASS_HIT : SPICE_CLASS_LORE, tile.ordinal, g))
         return;
-    up_tile<DT>(a, g, tile, red);
+    up_tile_kind<DT>(a, g, tile, red);
 }
 
 template <int DT>
@@ -44,8 +44,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         return;
     if (tile.kind == kKindLore)
         lore_down_tile<DT>(a, g.e, g.start, g.n, tile.rt, reinterpret_cast<float*>(&red[0][0][0][0]));
+    else if (tile.kind == kKindHit)
+        down_tile<DT, kKindHit>(a, g, tile.rt, red);
     else
-        down_tile<DT>(a, g, tile, red);
+        down_tile<DT, kKindShared>(a, g, tile.rt, red);
 }
 
 }  // namespace

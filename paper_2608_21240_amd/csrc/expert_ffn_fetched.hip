@@ -49,7 +49,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
             if (s >= 0 && s < a.T * a.K) f.slot_class[s] = SPICE_CLASS_EXACT_GPU;
         }
     }
-    up_tile<DT>(a, g, tile, red);
+    up_tile<DT, kKindHit>(a, g, tile.rt, a.perm + g.start, red);
 }
 
 template <int DT>
@@ -62,7 +62,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     tile.rt = blockIdx.x % tiles;
     Group g;
     if (!find_fetched_group(a, f, tile.ordinal, g)) return;
-    down_tile<DT>(a, g, tile, red);
+    down_tile<DT, kKindHit>(a, g, tile.rt, red);
 }
 
 }  // namespace

@@ -367,10 +367,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     if (tile.kind != kKindShared &&
         !find_group(a, tile.kind == kKindHit ? SPICE_CLASS_HIT : SPICE_CLASS_LORE, tile.ordinal, g))
         return;
+    auto& red = *reinterpret_cast<f32x4_t(*)[kWaves][kTokTiles][2][64]>(lds);
     if (tile.kind == kKindHit)
         mx_up_tile<kMxUpR>(a, g, tile, *reinterpret_cast<MxUpLds<kMxUpR>*>(lds));
+    else if (tile.kind == kKindShared)
+        up_tile<SPICE_BF16, kKindShared>(a, g, tile.rt, nullptr, red);
     else
-        up_tile<SPICE_BF16>(a, g, tile, *reinterpret_cast<f32x4_t(*)[kWaves][kTokTiles][2][64]>(lds));
+        up_tile<SPICE_BF16, kKindLore>(a, g, tile.rt, a.perm + g.start, red);
 }
 
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void ffn_down_mx_kernel(FfnArgs a,
@@ -387,7 +390,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     else if (tile.kind == kKindHit)
         mx_down_tile<kMxDownR>(a, g, tile, *reinterpret_cast<MxDownLds<kMxDownR>*>(lds));
     else
-        down_tile<SPICE_BF16>(a, g, tile, *reinterpret_cast<f32x4_t(*)[kWaves][kDownRows][kTokTiles][64]>(lds));
+        down_tile<SPICE_BF16, kKindShared>(a, g, tile.rt,
+                                           *reinterpret_cast<f32x4_t(*)[kWaves][kDownRows][kTokTiles][64]>(lds));
 }
 
 }  // namespace

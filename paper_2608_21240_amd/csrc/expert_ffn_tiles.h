@@ -83,7 +83,7 @@ struct Group {
 
 // The j-th expert (ascending id) whose bucket of class c is non-empty; for HIT
 // buckets its pool slot is fetched in the same round trip as the offsets.
-__device__ bool find_group(const FfnArgs& a, int c, int j, Group& g) {
+__device__ __attribute__((unused)) bool find_group(const FfnArgs& a, int c, int j, Group& g) {
     const int lane = threadIdx.x & 63;
     const int32_t* off = a.offsets + c * (a.N + 1);
     const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
@@ -316,12 +316,13 @@ __device__ __forceinline__ void wave_product(const char* const (&a)[NA], const c
 // ---------------------------------------------------------------------------
 // up: gate/up SwiGLU rows (HIT, shared) or A_e rows (LORE)
 // ---------------------------------------------------------------------------
-// Token ids of bucket positions p0 and p1 (p1 only with two token tiles): both loads go
-// out before either is checked.  Garbage in perm gives token 0 and a flag.
+// Token ids of bucket entries i0 and i1 (i1 only with two token tiles), from the bucket's
+// slot ids (global perm or an LDS list): both loads go out before either is checked.
+// Garbage gives token 0 and a flag.
 template <int NB>
-__device__ __forceinline__ void token_ids(const FfnArgs& a, int p0, int p1, int& t0, int& t1) {
-    const int s0 = a.perm[p0];
-    const int s1 = (NB == 2) ? a.perm[p1] : 0;
+__device__ __forceinline__ void token_ids(const FfnArgs& a, const int32_t* ids, int i0, int i1, int& t0, int& t1) {
+    const int s0 = ids[i0];
+    const int s1 = (NB == 2) ? ids[i1] : 0;
     __builtin_amdgcn_sched_barrier(0);  // both loads out before the first wait
     const int TK = a.T * a.K;
     const bool bad0 = s0 < 0 || s0 >= TK, bad1 = (NB == 2) && (s1 < 0 || s1 >= TK);
@@ -331,11 +332,12 @@ __device__ __forceinline__ void token_ids(const FfnArgs& a, int p0, int p1, int&
 }
 
 // One token group of an up tile: the weight loads of the first group go out, then the
-// token ids are read (bucket tiles) and the product runs.
+// token ids are read (ids != nullptr: a bucket; nullptr: tokens 0..T-1 in order) and the
+// product runs.
 template <int DT, int NB, bool kUp>
-__device__ __forceinline__ void up_pass(const FfnArgs& a, const char* gate, const char* up, bool bucket, int start,
-                                        int gi0, int gi1, size_t kb, int w, int quad,
-                                        f32x4_t (&red)[kWaves][kTokTiles][2][64], int lane) {
+__device__ __forceinline__ void up_pass(const FfnArgs& a, const char* gate, const char* up, const int32_t* ids, int gi0,
+                                        int gi1, size_t kb, int w, int quad, f32x4_t (&red)[kWaves][kTokTiles][2][64],
+                                        int lane) {
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
     constexpr int NA = kUp ? 2 : 1;
     constexpr int U = SPICE_GROUP_STEPS(NA, NB);
@@ -346,7 +348,7 @@ __device__ __forceinline__ void up_pass(const FfnArgs& a, const char* gate, cons
     mma_first_a<DT, NA, NB>(p, a.d, w, a0);
     __builtin_amdgcn_sched_barrier(0);
     int t0 = gi0, t1 = gi1;
-    if (bucket) token_ids<NB>(a, start + gi0, start + gi1, t0, t1);
+    if (ids) token_ids<NB>(a, ids, gi0, gi1, t0, t1);
     const char* xn[NB];
     xn[0] = static_cast<const char*>(a.x) + (size_t)t0 * a.d * es + kb;
     if constexpr (NB == 2) xn[1] = static_cast<const char*>(a.x) + (size_t)t1 * a.d * es + kb;
@@ -359,27 +361,38 @@ __device__ __forceinline__ void up_pass(const FfnArgs& a, const char* gate, cons
     }
 }
 
-template <int DT>
-__device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x4_t (&red)[kWaves][kTokTiles][2][64]) {
+// Up tile rt of one group, the kind fixed at compile time (so is the weight base: no tile
+// chooses it at run time).  KIND = kKindHit: 16 W1 rows and the same 16 W3 rows of the
+// group's pool slot, H = silu(X W1^T) * (X W3^T) to a.h at the bucket positions;
+// kKindShared: the same of the shared block for tokens 0..T-1, to a.hs; kKindLore: 16 rows
+// of A_e, U = X A_e^T to a.u at the bucket positions.  ids: the group's slot ids in bucket
+// order (its start is g.start), unused for kKindShared.
+template <int DT, int KIND>
+__device__ void up_tile(const FfnArgs& a, const Group& g, int rt, const int32_t* ids,
+                        f32x4_t (&red)[kWaves][kTokTiles][2][64]) {
     using T_ = Tr<DT>;
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
+    constexpr bool kUp = KIND != kKindLore;
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
     const void* wbase;
     size_t gate_row0, up_row0;
-    int nrows, start = 0, n = a.T;
-    if (tile.kind == kKindHit) {
+    int nrows, start, n;
+    if constexpr (KIND == kKindHit) {
         start = g.start;
         n = g.n;
         wbase = a.w13_pool;
         nrows = a.I;
         gate_row0 = (size_t)g.slot * 2 * a.I;
         up_row0 = gate_row0 + a.I;
-    } else if (tile.kind == kKindShared) {
+    } else if constexpr (KIND == kKindShared) {
+        start = 0;
+        n = a.T;
         wbase = a.w13s;
         nrows = a.Is;
         gate_row0 = 0;
         up_row0 = a.Is;
+        ids = nullptr;
     } else {
         start = g.start;
         n = g.n;
@@ -391,7 +404,7 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
     const int m = lane & 15;  // A row / B column owned by this lane
     const int quad = lane >> 4;
     // rows past the end of the matrix read its last row; their outputs are dropped
-    const int row = min(tile.rt * 16 + m, nrows - 1);
+    const int row = min(rt * 16 + m, nrows - 1);
     const size_t kb = (size_t)quad * T_::kLaneK * es;  // lane's byte offset inside a step
     const char* gate = static_cast<const char*>(wbase) + (gate_row0 + row) * (size_t)a.d * es + kb;
     const char* up = static_cast<const char*>(wbase) + (up_row0 + row) * (size_t)a.d * es + kb;
@@ -400,35 +413,29 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
         // padding columns read the bucket's last token; their outputs are dropped
         const int gi0 = min(g0 + m, n - 1), gi1 = min(g0 + 16 + m, n - 1);
-        const bool bucket = tile.kind != kKindShared;  // shared tiles take tokens 0..T-1 in order
-        if (tile.kind == kKindLore) {
-            if (ntt == 1) up_pass<DT, 1, false>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
-            else up_pass<DT, 2, false>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
-        } else {
-            if (ntt == 1) up_pass<DT, 1, true>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
-            else up_pass<DT, 2, true>(a, gate, up, bucket, start, gi0, gi1, kb, w, quad, red, lane);
-        }
+        if (ntt == 1) up_pass<DT, 1, kUp>(a, gate, up, ids, gi0, gi1, kb, w, quad, red, lane);
+        else up_pass<DT, 2, kUp>(a, gate, up, ids, gi0, gi1, kb, w, quad, red, lane);
         __syncthreads();
         if (w < ntt) {
             const int tt = w;
-            f32x4_t sg = red[0][tt][0][lane], su = red[0][tt][1][lane];
+            f32x4_t sg = red[0][tt][0][lane];
 #pragma unroll
-            for (int ww = 1; ww < kWaves; ++ww) {
-                sg += red[ww][tt][0][lane];
-                if (tile.kind != kKindLore) su += red[ww][tt][1][lane];
-            }
+            for (int ww = 1; ww < kWaves; ++ww) sg += red[ww][tt][0][lane];
             const int gi = g0 + tt * 16 + m;  // output column = token of lane m
-            const int orow = tile.rt * 16 + quad * 4;
-            if (gi < n && orow < nrows) {
-                if (tile.kind == kKindLore) {
-                    *reinterpret_cast<f32x4_t*>(a.u + (size_t)(start + gi) * a.r + orow) = sg;
-                } else {
+            const int orow = rt * 16 + quad * 4;
+            if constexpr (KIND == kKindLore) {
+                if (gi < n && orow < nrows) *reinterpret_cast<f32x4_t*>(a.u + (size_t)(start + gi) * a.r + orow) = sg;
+            } else {
+                f32x4_t su = red[0][tt][1][lane];
+#pragma unroll
+                for (int ww = 1; ww < kWaves; ++ww) su += red[ww][tt][1][lane];
+                if (gi < n && orow < nrows) {
                     f32x4_t h;
                     h.x = silu(sg.x) * su.x;
                     h.y = silu(sg.y) * su.y;
                     h.z = silu(sg.z) * su.z;
                     h.w = silu(sg.w) * su.w;
-                    if (tile.kind == kKindHit)
+                    if constexpr (KIND == kKindHit)
                         T_::store4(a.h, (size_t)(start + gi) * a.ldh + orow, h);
                     else
                         T_::store4(a.hs, (size_t)gi * a.ldhs + orow, h);
@@ -439,6 +446,14 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, const Tile& tile, f32x
     }
 }
 
+// A tile of any kind (the kind read at run time selects one of the instantiations).
+template <int DT>
+__device__ __forceinline__ void up_tile_kind(const FfnArgs& a, const Group& g, const Tile& tile,
+                                             f32x4_t (&red)[kWaves][kTokTiles][2][64]) {
+    if (tile.kind == kKindHit) up_tile<DT, kKindHit>(a, g, tile.rt, a.perm + g.start, red);
+    else if (tile.kind == kKindShared) up_tile<DT, kKindShared>(a, g, tile.rt, nullptr, red);
+    else up_tile<DT, kKindLore>(a, g, tile.rt, a.perm + g.start, red);
+}
 
 // ---------------------------------------------------------------------------
 // down: W2 rows (HIT, shared) with the MFMA path, B_e rows (LORE) on vector ALUs
@@ -525,33 +540,39 @@ __device__ __forceinline__ void down_pass(const char* const (&a)[NA], const char
         for (int j = 0; j < NB; ++j) red[w][rr][j][lane] = acc[rr][j];
 }
 
-template <int DT>
-__device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
-                          f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64]) {
+// Down tile rt (kDownRows x 16 rows of W2) of one group, the kind fixed at compile time:
+// kKindHit reads H at the bucket positions and writes y_slots there; kKindShared reads the
+// shared intermediate for tokens 0..T-1 and writes y_shared (times sgate[t] when set).
+template <int DT, int KIND>
+__device__ void down_tile(const FfnArgs& a, const Group& g, int rt, f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64]) {
+    static_assert(KIND == kKindHit || KIND == kKindShared, "down tiles are HIT or shared");
     using T_ = Tr<DT>;
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
     const void* wbase;
     const void* hbase;
-    int kdim, start = 0, n = a.T;
-    size_t row0;
-    if (tile.kind == kKindHit) {
+    int kdim, start, n;
+    size_t row0, ld;
+    if constexpr (KIND == kKindHit) {
         start = g.start;
         n = g.n;
         wbase = a.w2_pool;
         hbase = a.h;
         kdim = a.I;
         row0 = (size_t)g.slot * a.d;
+        ld = a.ldh;
     } else {
+        start = 0;
+        n = a.T;
         wbase = a.w2s;
         hbase = a.hs;
         kdim = a.Is;
         row0 = 0;
+        ld = a.ldhs;
     }
     const int m = lane & 15, quad = lane >> 4;
-    const int nrt = kDownRows;
-    const int dim0 = tile.rt * 16 * kDownRows;
+    const int dim0 = rt * 16 * kDownRows;
     const size_t kb = (size_t)quad * T_::kLaneK * es;
     const char* const aw[kDownRows] = {
         // tail rows read the last row; their outputs are dropped
@@ -559,40 +580,33 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, const Tile& tile,
         static_cast<const char*>(wbase) + (row0 + min(dim0 + 16 + m, a.d - 1)) * (size_t)kdim * es + kb};
     for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
-        const int hs0 = (tile.kind == kKindShared) ? 0 : start;
-        const size_t ld = (tile.kind == kKindShared) ? a.ldhs : a.ldh;
         const char* const hb[kTokTiles] = {
-            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + m, n - 1)) * ld * es + kb,
-            static_cast<const char*>(hbase) + (size_t)(hs0 + min(g0 + 16 + m, n - 1)) * ld * es + kb};
-        const char* const a1[1] = {aw[0]};
+            static_cast<const char*>(hbase) + (size_t)(start + min(g0 + m, n - 1)) * ld * es + kb,
+            static_cast<const char*>(hbase) + (size_t)(start + min(g0 + 16 + m, n - 1)) * ld * es + kb};
         const char* const h1[1] = {hb[0]};
-        if (nrt == 1) {
-            if (ntt == 1) down_pass<DT, 1, 1>(a1, h1, kdim, w, quad, red, lane);
-            else down_pass<DT, 1, 2>(a1, hb, kdim, w, quad, red, lane);
-        } else {
-            if (ntt == 1) down_pass<DT, kDownRows, 1>(aw, h1, kdim, w, quad, red, lane);
-            else down_pass<DT, kDownRows, 2>(aw, hb, kdim, w, quad, red, lane);
-        }
+        if (ntt == 1) down_pass<DT, kDownRows, 1>(aw, h1, kdim, w, quad, red, lane);
+        else down_pass<DT, kDownRows, 2>(aw, hb, kdim, w, quad, red, lane);
         __syncthreads();
         // wave w finalises (row tile, token tile) pair w
         const int rr = w % kDownRows, tt = w / kDownRows;
-        if (tt < ntt && rr < nrt) {
+        if (tt < ntt) {
             f32x4_t s = red[0][rr][tt][lane];
 #pragma unroll
             for (int ww = 1; ww < kWaves; ++ww) s += red[ww][rr][tt][lane];
             const int gi = g0 + tt * 16 + m;
             const int dim = dim0 + rr * 16 + quad * 4;
             if (gi < n && dim < a.d) {
-                float* dst = (tile.kind == kKindShared) ? a.y_shared + (size_t)gi * a.d
-                                                        : a.y_slots + (size_t)(start + gi) * a.d;
-                if (tile.kind == kKindShared && a.sgate) s *= a.sgate[gi];  // gated shared block
-                *reinterpret_cast<f32x4_t*>(dst + dim) = s;
+                if constexpr (KIND == kKindShared) {
+                    if (a.sgate) s *= a.sgate[gi];  // gated shared block
+                    *reinterpret_cast<f32x4_t*>(a.y_shared + (size_t)gi * a.d + dim) = s;
+                } else {
+                    *reinterpret_cast<f32x4_t*>(a.y_slots + (size_t)(start + gi) * a.d + dim) = s;
+                }
             }
         }
         __syncthreads();
     }
 }
-
 
 }  // namespace
 }  // namespace spice

@@ -43,7 +43,9 @@ class Pool {
     }
 
     // Runs fn(task) for every task in [0, n_tasks) on at most `threads` threads
-    // (the caller included).
+    // (the caller included).  A task that throws stops the handing out of further tasks;
+    // run() returns only after every thread has left fn (which lives in the caller's
+    // frame) and then rethrows the first exception on the calling thread.
     void run(int n_tasks, int threads, const std::function<void(int)>& fn) {
         std::lock_guard<std::mutex> region(region_mu_);
         threads = std::max(1, std::min(threads, n_tasks));
@@ -55,13 +57,20 @@ class Pool {
             next_.store(0);
             helpers_ = threads - 1;
             pending_ = threads - 1;
+            error_ = nullptr;
             ++generation_;
         }
         cv_.notify_all();
         work();
-        std::unique_lock<std::mutex> lk(mu_);
-        done_cv_.wait(lk, [&] { return pending_ == 0; });
-        fn_ = nullptr;
+        std::exception_ptr err;
+        {
+            std::unique_lock<std::mutex> lk(mu_);
+            done_cv_.wait(lk, [&] { return pending_ == 0; });
+            fn_ = nullptr;
+            err = error_;
+            error_ = nullptr;
+        }
+        if (err) std::rethrow_exception(err);
     }
 
     ~Pool() {
@@ -79,7 +88,13 @@ class Pool {
         for (;;) {
             const int task = next_.fetch_add(1);
             if (task >= n_tasks_) break;
-            (*fn_)(task);
+            try {
+                (*fn_)(task);
+            } catch (...) {
+                std::lock_guard<std::mutex> lk(mu_);
+                if (!error_) error_ = std::current_exception();
+                next_.store(n_tasks_);  // hand out no further task
+            }
         }
     }
 
@@ -117,6 +132,7 @@ class Pool {
     int n_tasks_ = 0, helpers_ = 0, pending_ = 0;
     uint64_t generation_ = 0;
     bool stop_ = false;
+    std::exception_ptr error_;  // first exception of the current region (guarded by mu_)
 };
 
 // ------------------------------------------------------------ dot products

@@ -2,6 +2,7 @@
 // Every entry point validates on the host before it touches HIP, returns a
 // status and never throws across the ABI.
 #include <algorithm>
+#include <chrono>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -108,6 +109,39 @@ spice_status_t gpu_address(const void* p, bool host_only, const char* name, void
                                                                    : ": not device or pinned host memory"));
 }
 
+// Device-visible addresses of the caller's pinned host copies (each optional).
+spice_status_t resolve_host_out(const spice_host_out_t* host_out, spice::RouteArgs& a) {
+    if (!host_out) return SPICE_OK;
+    spice_status_t st;
+    void* d = nullptr;
+    if (host_out->x) {
+        if ((st = gpu_address(host_out->x, true, "host_out.x", &d)) != SPICE_OK) return st;
+        a.hx = d;
+    }
+    if (host_out->topk_idx) {
+        if ((st = gpu_address(host_out->topk_idx, true, "host_out.topk_idx", &d)) != SPICE_OK) return st;
+        a.h_idx = static_cast<int32_t*>(d);
+    }
+    if (host_out->topk_w) {
+        if ((st = gpu_address(host_out->topk_w, true, "host_out.topk_w", &d)) != SPICE_OK) return st;
+        a.h_w = static_cast<float*>(d);
+    }
+    if (host_out->slot_class) {
+        if ((st = gpu_address(host_out->slot_class, true, "host_out.slot_class", &d)) != SPICE_OK) return st;
+        a.h_cls = static_cast<uint8_t*>(d);
+    }
+    if (host_out->class_counts) {
+        if ((st = gpu_address(host_out->class_counts, true, "host_out.class_counts", &d)) != SPICE_OK) return st;
+        a.h_counts = static_cast<int32_t*>(d);
+    }
+    if (host_out->ready) {
+        if ((st = gpu_address(host_out->ready, true, "host_out.ready", &d)) != SPICE_OK) return st;
+        a.h_ready = static_cast<uint32_t*>(d);
+        a.ready_value = host_out->ready_value;
+    }
+    return SPICE_OK;
+}
+
 #define SPICE_REQUIRE(ptr, name) \
     if (!(ptr)) return fail(SPICE_ERR_INVALID, name " is NULL")
 
@@ -172,12 +206,17 @@ spice_status_t spice_workspace_flags(void* ws, size_t ws_bytes, uint32_t* flags,
     SPICE_TRY_END
 }
 
-spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
-                                const float* logit_bias, const int32_t* resident_slot, const float* conf,
-                                double* logits, int32_t* topk_idx, float* topk_w, uint8_t* slot_class,
-                                int32_t* offsets, int32_t* perm, int32_t* inv_perm,
-                                const spice_host_out_t* host_out, void* ws, size_t ws_bytes, spice_stream_t stream) {
-    SPICE_TRY_BEGIN
+}  // extern "C"
+
+namespace {
+
+// Checks of a routing call and its kernel arguments (no launch).  T == 0 is valid; the
+// caller returns before launching.
+spice_status_t prep_route(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
+                          const float* logit_bias, const int32_t* resident_slot, const float* conf, double* logits,
+                          int32_t* topk_idx, float* topk_w, uint8_t* slot_class, int32_t* offsets, int32_t* perm,
+                          int32_t* inv_perm, const spice_host_out_t* host_out, void* ws, size_t ws_bytes,
+                          spice::RouteArgs& a) {
     spice_status_t st = check_cfg(cfg);
     if (st != SPICE_OK) return st;
     const spice_moe_cfg_t& c = *cfg;
@@ -196,7 +235,7 @@ spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const voi
     if ((st = check_ws(c, T, ws, ws_bytes)) != SPICE_OK) return st;
     const spice::WsLayout L = spice::ws_layout(c, T);
     char* wsb = static_cast<char*>(ws);
-    spice::RouteArgs a{};
+    a = spice::RouteArgs{};
     a.T = T; a.d = c.d; a.N = c.n_experts; a.K = c.top_k; a.C = c.n_slots; a.dtype = c.dtype;
     a.norm_topk = c.norm_topk; a.conf_mode = c.conf_mode; a.tau = c.tau;
     a.x = x; a.wg = w_gate; a.bias = logit_bias; a.resident_slot = resident_slot; a.conf = conf;
@@ -204,41 +243,41 @@ spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const voi
     a.topk_idx = topk_idx; a.topk_w = topk_w; a.slot_class = slot_class;
     a.offsets = offsets; a.perm = perm; a.inv_perm = inv_perm;
     a.ctrl = reinterpret_cast<uint32_t*>(wsb);
-    if (host_out) {
-        void* d = nullptr;
-        if (host_out->x) {
-            if ((st = gpu_address(host_out->x, true, "host_out.x", &d)) != SPICE_OK) return st;
-            a.hx = d;
-        }
-        if (host_out->topk_idx) {
-            if ((st = gpu_address(host_out->topk_idx, true, "host_out.topk_idx", &d)) != SPICE_OK) return st;
-            a.h_idx = static_cast<int32_t*>(d);
-        }
-        if (host_out->topk_w) {
-            if ((st = gpu_address(host_out->topk_w, true, "host_out.topk_w", &d)) != SPICE_OK) return st;
-            a.h_w = static_cast<float*>(d);
-        }
-        if (host_out->slot_class) {
-            if ((st = gpu_address(host_out->slot_class, true, "host_out.slot_class", &d)) != SPICE_OK) return st;
-            a.h_cls = static_cast<uint8_t*>(d);
-        }
-        if (host_out->class_counts) {
-            if ((st = gpu_address(host_out->class_counts, true, "host_out.class_counts", &d)) != SPICE_OK) return st;
-            a.h_counts = static_cast<int32_t*>(d);
-        }
-    }
+    a.wl_count = reinterpret_cast<int32_t*>(wsb) + spice::kWordWorkCount;
+    a.worklist = reinterpret_cast<int32_t*>(wsb) + spice::kWordWorkList;
+    return resolve_host_out(host_out, a);
+}
+
+}  // namespace
+
+extern "C" {
+
+spice_status_t moe_route_bucket(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
+                                const float* logit_bias, const int32_t* resident_slot, const float* conf,
+                                double* logits, int32_t* topk_idx, float* topk_w, uint8_t* slot_class,
+                                int32_t* offsets, int32_t* perm, int32_t* inv_perm,
+                                const spice_host_out_t* host_out, void* ws, size_t ws_bytes, spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    spice::RouteArgs a{};
+    const spice_status_t st = prep_route(cfg, T, x, w_gate, logit_bias, resident_slot, conf, logits, topk_idx, topk_w,
+                                         slot_class, offsets, perm, inv_perm, host_out, ws, ws_bytes, a);
+    if (st != SPICE_OK || T == 0) return st;
     hipError_t e = spice::launch_route_bucket(a, stream);
     if (e != hipSuccess) return hip_fail(e, "moe_route_bucket");
     return SPICE_OK;
     SPICE_TRY_END
 }
 
-static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
-                              const int32_t* offsets, const int32_t* resident_slot, const void* w13_pool,
-                              const void* w2_pool, const void* w13_shared, const void* w2_shared,
-                              const void* lore_A, const void* lore_B, float* y_slots, float* y_shared, void* ws,
-                              size_t ws_bytes, spice_stream_t stream, int groups, const char* name,
-                              const void* w_shared_gate = nullptr) {
+}  // extern "C"
+
+namespace {
+
+// Checks of a grouped-FFN call and its kernel arguments (no launch; T == 0 is valid).
+spice_status_t prep_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
+                        const int32_t* offsets, const int32_t* resident_slot, const void* w13_pool,
+                        const void* w2_pool, const void* w13_shared, const void* w2_shared, const void* lore_A,
+                        const void* lore_B, float* y_slots, float* y_shared, void* ws, size_t ws_bytes, int groups,
+                        const char* name, spice::FfnArgs& a) {
     spice_status_t st = check_cfg(cfg);
     if (st != SPICE_OK) return st;
     const spice_moe_cfg_t& c = *cfg;
@@ -275,7 +314,7 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
         return fail(SPICE_ERR_INVALID, std::string(name) + ": outputs alias each other or x");
     const spice::WsLayout L = spice::ws_layout(c, T);
     char* wsb = static_cast<char*>(ws);
-    spice::FfnArgs a{};
+    a = spice::FfnArgs{};
     a.T = T; a.d = c.d; a.N = c.n_experts; a.K = c.top_k; a.C = c.n_slots; a.I = c.inter;
     a.Is = c.shared_inter; a.r = c.lore_rank; a.dtype = c.dtype; a.groups = groups;
     a.ldh = c.inter + spice::kHPad; a.ldhs = c.shared_inter + spice::kHPad;
@@ -285,17 +324,39 @@ static spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void*
     a.h = wsb + L.h; a.hs = wsb + L.hs; a.u = reinterpret_cast<float*>(wsb + L.u);
     a.ctrl = reinterpret_cast<uint32_t*>(wsb);
     a.wfmt = c.wfmt;
-    if (w_shared_gate && (groups & spice::kDoShared) && c.shared_inter > 0) {
-        float* sg = reinterpret_cast<float*>(wsb + L.sgate);
-        hipError_t e = spice::launch_shared_gate(x, w_shared_gate, T, c.d, c.dtype, sg, stream);
-        if (e != hipSuccess) return hip_fail(e, name);
+    return SPICE_OK;
+}
+
+// The grouped FFN's launches: the shared block's gate first when it has one, then the
+// tiles (MXFP4 or dtype experts).
+hipError_t launch_ffn(spice::FfnArgs& a, const void* w_shared_gate, void* ws, const spice_moe_cfg_t& c,
+                      hipStream_t stream) {
+    if (w_shared_gate && (a.groups & spice::kDoShared) && c.shared_inter > 0) {
+        float* sg = reinterpret_cast<float*>(static_cast<char*>(ws) + spice::ws_layout(c, a.T).sgate);
+        hipError_t e = spice::launch_shared_gate(a.x, w_shared_gate, a.T, c.d, c.dtype, sg, stream);
+        if (e != hipSuccess) return e;
         a.sgate = sg;
     }
-    hipError_t e = c.wfmt == SPICE_WFMT_MXFP4 ? spice::launch_expert_ffn_mx(a, stream)
-                                                : spice::launch_expert_ffn(a, stream);
+    return c.wfmt == SPICE_WFMT_MXFP4 ? spice::launch_expert_ffn_mx(a, stream) : spice::launch_expert_ffn(a, stream);
+}
+
+spice_status_t run_ffn(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
+                       const int32_t* offsets, const int32_t* resident_slot, const void* w13_pool, const void* w2_pool,
+                       const void* w13_shared, const void* w2_shared, const void* lore_A, const void* lore_B,
+                       float* y_slots, float* y_shared, void* ws, size_t ws_bytes, spice_stream_t stream, int groups,
+                       const char* name, const void* w_shared_gate = nullptr) {
+    spice::FfnArgs a{};
+    const spice_status_t st = prep_ffn(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared,
+                                       w2_shared, lore_A, lore_B, y_slots, y_shared, ws, ws_bytes, groups, name, a);
+    if (st != SPICE_OK || T == 0) return st;
+    const hipError_t e = launch_ffn(a, w_shared_gate, ws, *cfg, stream);
     if (e != hipSuccess) return hip_fail(e, name);
     return SPICE_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 spice_status_t moe_expert_ffn_grouped(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const int32_t* perm,
                                       const int32_t* offsets, const int32_t* resident_slot, const void* w13_pool,
@@ -436,10 +497,14 @@ spice_status_t moe_spec_update(const spice_moe_cfg_t* cfg, int32_t T, int32_t de
     SPICE_TRY_END
 }
 
-spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w, const uint8_t* slot_class,
-                           const int32_t* inv_perm, const float* y_slots, const float* y_shared, const float* resid,
-                           void* out, spice_stream_t stream) {
-    SPICE_TRY_BEGIN
+}  // extern "C"
+
+namespace {
+
+// Checks of a combine call and its kernel arguments (no launch; T == 0 is valid).
+spice_status_t prep_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w, const uint8_t* slot_class,
+                            const int32_t* inv_perm, const float* y_slots, const float* y_shared, const float* resid,
+                            void* out, spice::CombineArgs& a) {
     spice_status_t st = check_cfg(cfg);
     if (st != SPICE_OK) return st;
     const spice_moe_cfg_t& c = *cfg;
@@ -457,13 +522,89 @@ spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* t
         return fail(SPICE_ERR_INVALID, "moe_combine: out aliases an input");
     void* resid_dev = nullptr;
     if (resid && (st = gpu_address(resid, false, "moe_combine: resid", &resid_dev)) != SPICE_OK) return st;
-    spice::CombineArgs a{};
+    a = spice::CombineArgs{};
     a.T = T; a.d = c.d; a.K = c.top_k; a.dtype = c.dtype;
     a.topk_w = topk_w; a.slot_class = slot_class; a.inv_perm = inv_perm; a.y_slots = y_slots;
     a.y_shared = y_shared; a.resid = static_cast<const float*>(resid_dev); a.out = out;
+    return SPICE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* topk_w, const uint8_t* slot_class,
+                           const int32_t* inv_perm, const float* y_slots, const float* y_shared, const float* resid,
+                           void* out, spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    spice::CombineArgs a{};
+    const spice_status_t st = prep_combine(cfg, T, topk_w, slot_class, inv_perm, y_slots, y_shared, resid, out, a);
+    if (st != SPICE_OK || T == 0) return st;
     hipError_t e = spice::launch_combine(a, stream);
     if (e != hipSuccess) return hip_fail(e, "moe_combine");
     return SPICE_OK;
+    SPICE_TRY_END
+}
+
+spice_status_t moe_layer_gpu(const spice_moe_cfg_t* cfg, int32_t T, const void* x, const void* w_gate,
+                             const float* logit_bias, const int32_t* resident_slot, const float* conf,
+                             const void* w13_pool, const void* w2_pool, const void* w13_shared, const void* w2_shared,
+                             const void* w_shared_gate, const void* lore_A, const void* lore_B, double* logits,
+                             int32_t* topk_idx, float* topk_w, uint8_t* slot_class, int32_t* offsets, int32_t* perm,
+                             int32_t* inv_perm, float* y_slots, float* y_shared, const spice_host_out_t* host_out,
+                             const float* resid, void* out, void* ws, size_t ws_bytes, spice_stream_t stream) {
+    SPICE_TRY_BEGIN
+    spice::RouteArgs r{};
+    spice_status_t st = prep_route(cfg, T, x, w_gate, logit_bias, resident_slot, conf, logits, topk_idx, topk_w,
+                                   slot_class, offsets, perm, inv_perm, host_out, ws, ws_bytes, r);
+    if (st != SPICE_OK || T == 0) return st;
+    const spice_moe_cfg_t& c = *cfg;
+    int groups = spice::kDoHit | spice::kDoShared;
+    if (lore_A && lore_B) groups |= spice::kDoLore;
+    spice::FfnArgs f{};
+    st = prep_ffn(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared, lore_A, lore_B,
+                  y_slots, y_shared, ws, ws_bytes, groups, "moe_layer_gpu", f);
+    if (st != SPICE_OK) return st;
+    spice::CombineArgs cb{};
+    if (out && (st = prep_combine(cfg, T, topk_w, slot_class, inv_perm, y_slots, y_shared, resid, out, cb)) != SPICE_OK)
+        return st;
+    const bool gated = w_shared_gate && c.shared_inter > 0;
+    hipError_t e;
+    if (c.wfmt == SPICE_WFMT_DTYPE && T <= spice::kRouteTokenMaxT && T * c.top_k <= spice::kLayerMaxSlots &&
+        !spice::expert_gemm_applies(f)) {
+        if (gated) {
+            float* sg = reinterpret_cast<float*>(static_cast<char*>(ws) + spice::ws_layout(c, T).sgate);
+            r.w_sg = w_shared_gate;
+            r.sgate = sg;
+            f.sgate = sg;
+        }
+        e = spice::launch_layer_decode(r, f, stream);
+    } else {
+        e = spice::launch_route_bucket(r, stream);
+        if (e == hipSuccess) e = launch_ffn(f, gated ? w_shared_gate : nullptr, ws, c, stream);
+    }
+    if (e == hipSuccess && out) e = spice::launch_combine(cb, stream);
+    if (e != hipSuccess) return hip_fail(e, "moe_layer_gpu");
+    return SPICE_OK;
+    SPICE_TRY_END
+}
+
+spice_status_t spice_wait_ready(const volatile uint32_t* ready, uint32_t value, int64_t timeout_us) {
+    SPICE_TRY_BEGIN
+    SPICE_REQUIRE(ready, "ready");
+    const auto t0 = std::chrono::steady_clock::now();
+    const int64_t limit = timeout_us > 0 ? timeout_us : 10000000;
+    for (uint64_t i = 0;; ++i) {
+        if (__atomic_load_n(ready, __ATOMIC_ACQUIRE) == value) return SPICE_OK;
+        if ((i & 255) == 255) {
+            const int64_t el =
+                std::chrono::duration_cast<std::chrono::microseconds>(std::chrono::steady_clock::now() - t0).count();
+            if (el > limit)
+                return fail(SPICE_ERR_HIP, "spice_wait_ready: the ready word did not reach " + std::to_string(value) +
+                                               " within " + std::to_string(limit) + " us");
+        }
+        __builtin_ia32_pause();
+    }
     SPICE_TRY_END
 }
 

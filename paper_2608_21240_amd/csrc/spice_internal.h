@@ -10,21 +10,19 @@
 namespace spice {
 
 // Workspace control region (32-bit words at the start of every workspace).
-constexpr int kWordFlags = 0;          // device flags, SPICE_FLAG_* (atomic OR)
-constexpr int kWordRouteDone = 1;      // route tiles finished (last one buckets)
-constexpr int kWordTileCounters = 64;  // one counter per route token tile
-constexpr int kRouteTok = 8;           // most tokens per route block
-constexpr int kRouteExp = 8;           // experts per route block (one per wave)
-constexpr int kRouteXLds = 65536;      // LDS bytes for the block's token rows
-constexpr int kRouteMinTok = 4;        // fewest tokens per route block (d * elem <= 16 KiB)
-static_assert((kWordTileCounters + SPICE_MAX_TOKENS / kRouteMinTok) * 4 <= SPICE_WS_CONTROL_BYTES,
-              "control region too small");
+constexpr int kWordFlags = 0;       // device flags, SPICE_FLAG_* (atomic OR)
+constexpr int kWordWorkCount = 16;  // [3] non-empty buckets per class (the work lists' lengths)
+constexpr int kWordWorkList = 1024; // [3][N] int4 work records {expert, pool slot, start, n}
+constexpr int kWordTokCount = 4096; // [T] arrivals of a token's routing blocks (T <= kRouteTokenMaxT)
+static_assert(kWordWorkList + 3 * SPICE_MAX_EXPERTS * 4 <= kWordTokCount, "work lists overlap the counters");
 
-// Tokens per route block for rows of d elements of es bytes.
-inline int route_tokens_per_block(int d, int es) {
-    const int tt = kRouteXLds / (d * es);
-    return tt > kRouteTok ? kRouteTok : tt;
-}
+// Largest T whose routing spreads each token's router rows over a few blocks (larger T:
+// the tiled logits kernel).
+constexpr int kRouteTokenMaxT = 256;
+static_assert((kWordTokCount + kRouteTokenMaxT) * 4 <= SPICE_WS_CONTROL_BYTES, "control region too small");
+// Most slots T*K of the fused decode-layer launches (layer_decode.hip); larger calls take
+// the separate routing, FFN and combine launches.
+constexpr int kLayerMaxSlots = 1024;
 
 // Row padding (elements) of the SwiGLU intermediates in the workspace: row strides
 // that are multiples of large powers of two put every row of a tile on the same
@@ -62,12 +60,18 @@ struct RouteArgs {
     int32_t* perm;
     int32_t* inv_perm;
     uint32_t* ctrl;       // workspace control words
+    int32_t* worklist;    // [3][N][4] work records (control region)
+    int32_t* wl_count;    // [3] their lengths (control region)
+    const void* w_sg;     // nullable: the shared block's gate row [d]; sgate[t] = sigmoid(w_sg . x[t])
+    float* sgate;         // [T], written when w_sg is set
     // device-visible addresses of the caller's pinned host copies (each nullable)
     void* hx;
     int32_t* h_idx;
     float* h_w;
     uint8_t* h_cls;
     int32_t* h_counts;
+    uint32_t* h_ready;    // nullable: receives ready_value once every host copy has landed
+    uint32_t ready_value;
 };
 
 // Bytes of one routed expert's W13 [2I][d] and W2 [d][I] in the cfg's weight format.
@@ -173,6 +177,9 @@ bool expert_gemm_applies(const FfnArgs& a);
 hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream_t s);
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
+// The fused decode layer (routing, bucketing, shared block, HIT and LoRE FFN) in three
+// launches; bf16/fp32 experts, T <= kRouteTokenMaxT, T*K <= kLayerMaxSlots.
+hipError_t launch_layer_decode(const RouteArgs& r, const FfnArgs& f, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 // The same launch with MXFP4 routed experts (expert_ffn_mx.hip).
 hipError_t launch_expert_ffn_mx(const FfnArgs& a, hipStream_t s);

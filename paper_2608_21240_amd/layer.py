@@ -6,9 +6,13 @@ block and every expert's LoRE factors, and keeps the non-resident experts on
 the host for the exact CPU path.  ``LayerRun`` owns the per-call buffers and
 runs the path in the order the paper describes (Sec. 4.3):
 
-    stream : route+bucket (also writes x and the routing into pinned host memory)
-             -> grouped FFN (+LoRE) ........................ -> combine (reads resid over PCIe)
-    host   :        wait(route) -> exact residual on CPU threads -> resid (pinned) ^
+    stream : moe_layer_gpu: routing + shared up | bucketing + shared down + routed up | routed down
+             (the bucketing block also writes x and the routing into pinned host memory, then
+             a ready word)  ........................................ -> combine (reads resid over PCIe)
+    host   :   wait(ready word) -> exact residual on CPU threads -> resid (pinned) ^
+
+With layer_call=False the same layer runs as the separate calls (moe_route_bucket,
+moe_expert_ffn_grouped, moe_combine) and the host waits for the routing call's event.
 
 Every arithmetic step runs inside libspice_moe (HIP kernels or its host path).
 """
@@ -166,8 +170,10 @@ class LayerRun:
     """Buffers and streams for layer calls with up to T tokens."""
 
     def __init__(self, shape, T: int, n_slots: int, tau: float = 0.5, conf_mode: int = 0, norm_topk: int = 0,
-                 device: str = "cuda", keep_logits: bool = False, fetch_slots: int = 0, wfmt: int = 0):
+                 device: str = "cuda", keep_logits: bool = False, fetch_slots: int = 0, wfmt: int = 0,
+                 layer_call: bool = True):
         self.shape, self.T = shape, T
+        self.layer_call = layer_call
         self.cfg = spice.make_cfg(shape, n_slots, tau, conf_mode, norm_topk, wfmt)
         s, K, N, d = shape, shape.top_k, shape.n_experts, shape.d
         i32 = dict(dtype=torch.int32, device=device)
@@ -194,8 +200,13 @@ class LayerRun:
         self.cls_host = torch.empty((T, K), dtype=torch.uint8).pin_memory()
         self.counts_host = torch.zeros(3, dtype=torch.int32).pin_memory()
         self.resid = torch.zeros((T, d), dtype=torch.float32).pin_memory()
-        self.host_out = spice.host_out(self.x_host, self.idx_host, self.w_host, self.cls_host, self.counts_host)
+        self.ready = torch.zeros(1, dtype=torch.int32).pin_memory()
+        self.epoch = 0
+        self.host_out = spice.host_out(self.x_host, self.idx_host, self.w_host, self.cls_host, self.counts_host,
+                                       self.ready, 0)
+        self.host_out_ev = spice.host_out(self.x_host, self.idx_host, self.w_host, self.cls_host, self.counts_host)
         self.e_route = torch.cuda.Event()
+        self.wait_ready = False  # the host waits for the ready word (layer call) or for e_route
         # fetch pool of the exact-miss split (Eq. 12: M_fetch), if any
         self.fetch_slots = fetch_slots
         if fetch_slots:
@@ -220,8 +231,28 @@ class LayerRun:
         T = self.T if T is None else T
         spice.moe_route_bucket(self.cfg, T, x, L.wg, L.bias, L.resident_slot, conf, self.logits, self.topk_idx,
                                self.topk_w, self.slot_class, self.offsets, self.perm, self.inv_perm,
-                               self.host_out if to_host else None, self.ws, self.ws_bytes)
+                               self.host_out_ev if to_host else None, self.ws, self.ws_bytes)
         self.e_route.record(torch.cuda.current_stream())
+        self.wait_ready = False
+
+    def layer_gpu(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
+                  to_host: bool = True, fuse_lore: bool = True, resid=None, out: bool = False):
+        """Routing, bucketing and the expert FFN (+ LoRE) as one library call (moe_layer_gpu);
+        with to_host the routing's host copies are followed by a new ready word; with out the
+        combine runs too, with resid (device or pinned host memory, or None)."""
+        T = self.T if T is None else T
+        ho = None
+        if to_host:
+            self.epoch = (self.epoch + 1) & 0x7FFFFFFF
+            self.host_out.ready_value = self.epoch
+            ho = self.host_out
+        la, lb = (L.lore_A, L.lore_B) if fuse_lore else (None, None)
+        spice.moe_layer_gpu(self.cfg, T, x, L.wg, L.bias, L.resident_slot, conf, L.w13_pool, L.w2_pool, L.w13s,
+                            L.w2s, L.w_sg, la, lb, self.logits, self.topk_idx, self.topk_w, self.slot_class,
+                            self.offsets, self.perm, self.inv_perm, self.y_slots, self.y_shared, ho, resid,
+                            self.out if out else None, self.ws, self.ws_bytes)
+        self.e_route.record(torch.cuda.current_stream())
+        self.wait_ready = to_host
 
     def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
         T = self.T if T is None else T
@@ -249,7 +280,10 @@ class LayerRun:
         """Wait for the route kernel's host copies; with a split cost model, fetch the experts
         the planner picks and queue their FFN on the GPU; then the CPU residual of the other
         exact misses into self.resid."""
-        self.e_route.synchronize()
+        if self.wait_ready:
+            spice.spice_wait_ready(self.ready, self.epoch)
+        else:
+            self.e_route.synchronize()
         if before_residual is not None:
             before_residual()
         self.last_fetch = []
@@ -290,12 +324,13 @@ class LayerRun:
         self.x_cur = x
         if "start" in ev:
             ev["start"].record()
-        self.route(L, x, conf, T, to_host=exact)
-        if "routed" in ev:
-            ev["routed"].record()
-        if "ffn0" in ev:
-            ev["ffn0"].record()
-        self.experts(L, x, T, fuse_lore=True)
+        if self.layer_call:
+            self.layer_gpu(L, x, conf, T, to_host=exact)
+        else:
+            self.route(L, x, conf, T, to_host=exact)
+            if "routed" in ev:
+                ev["routed"].record()
+            self.experts(L, x, T, fuse_lore=True)
         if "experts" in ev:
             ev["experts"].record()
         if after_experts is not None:

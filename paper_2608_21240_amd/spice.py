@@ -29,12 +29,12 @@ SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
 EXPORTS = (
     "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
     "moe_route_bucket", "moe_expert_ffn_grouped", "moe_expert_ffn_grouped_gated", "lore_surrogate_apply",
-    "moe_combine",
+    "moe_combine", "moe_layer_gpu",
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
     "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
     "moe_spec_update", "moe_prefetch_h_min", "moe_prefetch_queue", "moe_cache_prefetch",
     "spice_lore_fit_workspace_bytes", "moe_lore_fit",
-    "spice_status_string", "spice_last_error",
+    "spice_wait_ready", "spice_status_string", "spice_last_error",
 )
 
 
@@ -63,12 +63,15 @@ class spice_spec_host_t(ctypes.Structure):
 
 class spice_host_out_t(ctypes.Structure):
     _fields_ = [("x", ctypes.c_void_p), ("topk_idx", ctypes.c_void_p), ("topk_w", ctypes.c_void_p),
-                ("slot_class", ctypes.c_void_p), ("class_counts", ctypes.c_void_p)]
+                ("slot_class", ctypes.c_void_p), ("class_counts", ctypes.c_void_p), ("ready", ctypes.c_void_p),
+                ("ready_value", ctypes.c_uint32)]
 
 
-def host_out(x=None, topk_idx=None, topk_w=None, slot_class=None, class_counts=None) -> spice_host_out_t:
-    """Pinned host buffers (tensors, arrays or addresses) for moe_route_bucket's host copies."""
-    return spice_host_out_t(_p(x), _p(topk_idx), _p(topk_w), _p(slot_class), _p(class_counts))
+def host_out(x=None, topk_idx=None, topk_w=None, slot_class=None, class_counts=None, ready=None,
+             ready_value: int = 0) -> spice_host_out_t:
+    """Pinned host buffers (tensors, arrays or addresses) for the routing's host copies."""
+    return spice_host_out_t(_p(x), _p(topk_idx), _p(topk_w), _p(slot_class), _p(class_counts), _p(ready),
+                            ready_value & 0xFFFFFFFF)
 
 
 def make_cfg(shape, n_slots: int, tau: float = 0.5, conf_mode: int = SPICE_CONF_INPUT,
@@ -99,6 +102,7 @@ def lib() -> ctypes.CDLL:
                                                   _P]),
             "lore_surrogate_apply": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
             "moe_combine": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
+            "moe_layer_gpu": (_I, [C, _I] + [_P] * 21 + [ctypes.POINTER(spice_host_out_t), _P, _P, _P, _Z, _P]),
             "moe_exact_residual_host": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I]),
             "moe_cache_create": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _I, _P, ctypes.POINTER(_P)]),
             "moe_cache_step": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, ctypes.POINTER(_I), _P, _P]),
@@ -118,6 +122,7 @@ def lib() -> ctypes.CDLL:
             "spice_lore_fit_workspace_bytes": (_Z, [C, _I, _I]),
             "moe_lore_fit": (_I, [C, _I, _I, _P, _P, _P, _P, _P, _P, _P, _P, ctypes.POINTER(ctypes.c_double), _P, _Z,
                                   _P]),
+            "spice_wait_ready": (_I, [_P, ctypes.c_uint32, ctypes.c_int64]),
             "spice_status_string": (ctypes.c_char_p, [_I]),
             "spice_last_error": (ctypes.c_char_p, []),
         }
@@ -164,6 +169,11 @@ def last_error() -> str:
 
 def spice_status_string(status: int) -> str:
     return lib().spice_status_string(status).decode()
+
+
+def spice_wait_ready(ready, value: int, timeout_us: int = 0) -> None:
+    """Wait on the host until the pinned word `ready` holds `value`."""
+    _check("spice_wait_ready", lib().spice_wait_ready(_p(ready), value & 0xFFFFFFFF, timeout_us))
 
 
 def spice_workspace_bytes(cfg: spice_moe_cfg_t, T: int) -> int:
@@ -216,6 +226,18 @@ def moe_combine(cfg, T, topk_w, slot_class, inv_perm, y_slots, y_shared, resid, 
     _check("moe_combine", lib().moe_combine(
         ctypes.byref(cfg), T, _p(topk_w), _p(slot_class), _p(inv_perm), _p(y_slots), _p(y_shared), _p(resid),
         _p(out), _stream(stream)))
+
+
+def moe_layer_gpu(cfg, T, x, w_gate, logit_bias, resident_slot, conf, w13_pool, w2_pool, w13_shared, w2_shared,
+                  w_shared_gate, lore_A, lore_B, logits, topk_idx, topk_w, slot_class, offsets, perm, inv_perm,
+                  y_slots, y_shared, host_out: Optional[spice_host_out_t], resid, out, ws, ws_bytes,
+                  stream=None) -> None:
+    _check("moe_layer_gpu", lib().moe_layer_gpu(
+        ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(w13_pool),
+        _p(w2_pool), _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(logits),
+        _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm), _p(y_slots), _p(y_shared),
+        None if host_out is None else ctypes.byref(host_out), _p(resid), _p(out), _p(ws), ws_bytes,
+        _stream(stream)))
 
 
 def moe_exact_residual_host(cfg, T, x_host, topk_idx_host, topk_w_host, slot_class_host,

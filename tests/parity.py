@@ -64,13 +64,17 @@ class Case:
 
     # ---------------------------------------------------------------- HIP path
     def run_gpu(self, dev: Optional[LY.DeviceLayer] = None, fused: bool = True, exact: bool = True,
-                run: Optional[LY.LayerRun] = None, n_threads: int = 0, split=None, fetch_slots: int = 0):
+                run: Optional[LY.LayerRun] = None, n_threads: int = 0, split=None, fetch_slots: int = 0,
+                layer_call: bool = True):
+        """fused: the whole layer through LayerRun.forward (moe_layer_gpu when layer_call, else the
+        separate routing and FFN calls); not fused: routing, FFN without LoRE, lore_surrogate_apply,
+        the host residual and the combine as separate calls."""
         s = self.shape
         self.dev = dev if dev is not None else LY.DeviceLayer(self.host, n_slots=self.n_slots)
         self.run = run if run is not None else LY.LayerRun(s, self.T, self.dev.C, tau=self.wl.tau,
                                                             conf_mode=self.wl.conf_mode, norm_topk=self.wl.norm_topk,
                                                             keep_logits=True, fetch_slots=fetch_slots,
-                                                            wfmt=self.wl.wfmt)
+                                                            wfmt=self.wl.wfmt, layer_call=layer_call)
         R = self.run
         xd = LY.to_tensor(self.x, s.dtype, "cuda")
         conf = torch.from_numpy(np.ascontiguousarray(self.conf)).cuda()

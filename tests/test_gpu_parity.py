@@ -45,13 +45,14 @@ def test_tiny_f32_layer(fused):
     c.check_outputs()
 
 
+@pytest.mark.parametrize("layer_call", [True, False])
 @pytest.mark.parametrize("shape,T,R", [(RAGGED_BF16, 37, 6), (RAGGED_BF16, 5, 9), (RAGGED_F32, 41, 4),
                                        (W.small_shape(), 70, 5)])
-def test_ragged_layers(shape, T, R):
+def test_ragged_layers(shape, T, R, layer_call):
     say(f"ragged d={shape.d} N={shape.n_experts} K={shape.top_k} I={shape.inter} Is={shape.shared_inter} "
-        f"r={shape.lore_rank} T={T} R={R}")
+        f"r={shape.lore_rank} T={T} R={R} layer_call={layer_call}")
     c = Case(small_wl(shape, T, R))
-    c.run_gpu()
+    c.run_gpu(layer_call=layer_call)
     c.run_oracle()
     c.check_routing()
     c.check_outputs()
@@ -67,12 +68,13 @@ def dsv2():
     return wl, host, dev
 
 
+@pytest.mark.parametrize("layer_call", [True, False])
 @pytest.mark.parametrize("T", [1, 8, 32])
-def test_dsv2_decode(dsv2, T):
+def test_dsv2_decode(dsv2, T, layer_call):
     wl, host, dev = dsv2
-    say(f"dsv2 decode T={T}")
+    say(f"dsv2 decode T={T} layer_call={layer_call}")
     c = Case(wl.with_(tokens=T), host=host)
-    c.run_gpu(dev=dev)
+    c.run_gpu(dev=dev, layer_call=layer_call)
     c.run_oracle()
     c.check_routing()
     c.check_outputs()
@@ -212,13 +214,14 @@ def test_repeat_runs_are_bit_identical():
             assert np.array_equal(g1[k], g2[k]), k
 
 
+@pytest.mark.parametrize("layer_call", [True, False])
 @pytest.mark.parametrize("shape,T,R", [(RAGGED_BF16, 37, 6), (RAGGED_F32, 41, 4)])
-def test_host_copies_match_device_outputs(shape, T, R):
-    """The route kernel's pinned-host copies equal its device outputs and the input x;
+def test_host_copies_match_device_outputs(shape, T, R, layer_call):
+    """The bucketing block's pinned-host copies equal the device outputs and the input x;
     the class counts equal the histogram of the classes."""
-    say(f"host copies d={shape.d} T={T}")
+    say(f"host copies d={shape.d} T={T} layer_call={layer_call}")
     c = Case(small_wl(shape, T, R))
-    c.run_gpu()
+    c.run_gpu(layer_call=layer_call)
     run = c.run
     assert np.array_equal(run.idx_host[:T].numpy(), c.g["idx"])
     assert np.array_equal(run.w_host[:T].numpy(), c.g["w"])
