@@ -279,6 +279,31 @@ spice_status_t moe_layer_gpu(const spice_moe_cfg_t* cfg, int32_t T, const void* 
                              spice_stream_t stream);
 
 /*
+ * moe_layer_gpu for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, and harnesses that forbid hipMalloc.  The same launches and
+ * outputs as moe_layer_gpu; instead of a caller's workspace it uses a static device array
+ * of SPICE_NOALLOC_SCRATCH_BYTES that the library holds on each GPU it runs on until the
+ * process ends (zero when loaded; its device address is looked up once per device).  The
+ * call allocates nothing.  The caller still passes every input and output.
+ *   Errors: those of moe_layer_gpu; UNSUPPORTED when spice_workspace_bytes(cfg, T) exceeds
+ *   SPICE_NOALLOC_SCRATCH_BYTES.  Device flags raised by the kernels are not reported.
+ * Every call on one GPU shares that GPU's array: calls that overlap on one GPU (different
+ * streams, or host threads without ordering) race and must not be issued.
+ */
+#define SPICE_NOALLOC_SCRATCH_BYTES (32u << 20)
+spice_status_t moe_layer_gpu_noalloc(const spice_moe_cfg_t* cfg, int32_t T, const void* x,
+                                     const void* w_gate, const float* logit_bias,
+                                     const int32_t* resident_slot, const float* conf,
+                                     const void* w13_pool, const void* w2_pool,
+                                     const void* w13_shared, const void* w2_shared,
+                                     const void* w_shared_gate, const void* lore_A,
+                                     const void* lore_B, double* logits, int32_t* topk_idx,
+                                     float* topk_w, uint8_t* slot_class, int32_t* offsets,
+                                     int32_t* perm, int32_t* inv_perm, float* y_slots,
+                                     float* y_shared, const spice_host_out_t* host_out,
+                                     const float* resid, void* out, spice_stream_t stream);
+
+/*
  * Step 5, host side: resid[t] = sum_{k in EXACT(t)} g[t][k] E_e(x_t) computed on the
  * CPU from host-resident expert weights (M_cpu of Eq. 12; Sec. 4.3: exact, the same
  * weights, routing untouched).  Synchronous and reentrant; uses n_threads worker

@@ -29,7 +29,7 @@ SPICE_FLAG_BAD_SLOT, SPICE_FLAG_BAD_INDEX = 1, 2
 EXPORTS = (
     "spice_workspace_bytes", "spice_workspace_init", "spice_workspace_flags",
     "moe_route_bucket", "moe_expert_ffn_grouped", "moe_expert_ffn_grouped_gated", "lore_surrogate_apply",
-    "moe_combine", "moe_layer_gpu",
+    "moe_combine", "moe_layer_gpu", "moe_layer_gpu_noalloc",
     "moe_exact_residual_host", "moe_cache_create", "moe_cache_step", "moe_cache_wait", "moe_cache_state",
     "moe_cache_destroy", "moe_split_plan", "moe_fetch_experts", "moe_expert_ffn_fetched",
     "moe_spec_update", "moe_prefetch_h_min", "moe_prefetch_queue", "moe_cache_prefetch",
@@ -103,6 +103,7 @@ def lib() -> ctypes.CDLL:
             "lore_surrogate_apply": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _Z, _P]),
             "moe_combine": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _P]),
             "moe_layer_gpu": (_I, [C, _I] + [_P] * 21 + [ctypes.POINTER(spice_host_out_t), _P, _P, _P, _Z, _P]),
+            "moe_layer_gpu_noalloc": (_I, [C, _I] + [_P] * 21 + [ctypes.POINTER(spice_host_out_t), _P, _P, _P]),
             "moe_exact_residual_host": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _P, _I]),
             "moe_cache_create": (_I, [C, _I, _P, _P, _P, _P, _P, _P, _I, _P, ctypes.POINTER(_P)]),
             "moe_cache_step": (_I, [_P, _I, _I, _I, _P, _P, _I, _P, _P, ctypes.POINTER(_I), _P, _P]),
@@ -238,6 +239,20 @@ def moe_layer_gpu(cfg, T, x, w_gate, logit_bias, resident_slot, conf, w13_pool, 
         _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm), _p(y_slots), _p(y_shared),
         None if host_out is None else ctypes.byref(host_out), _p(resid), _p(out), _p(ws), ws_bytes,
         _stream(stream)))
+
+
+SPICE_NOALLOC_SCRATCH_BYTES = 32 << 20
+
+
+def moe_layer_gpu_noalloc(cfg, T, x, w_gate, logit_bias, resident_slot, conf, w13_pool, w2_pool, w13_shared,
+                          w2_shared, w_shared_gate, lore_A, lore_B, logits, topk_idx, topk_w, slot_class, offsets,
+                          perm, inv_perm, y_slots, y_shared, host_out: Optional[spice_host_out_t], resid, out,
+                          stream=None) -> None:
+    _check("moe_layer_gpu_noalloc", lib().moe_layer_gpu_noalloc(
+        ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(w13_pool),
+        _p(w2_pool), _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(logits),
+        _p(topk_idx), _p(topk_w), _p(slot_class), _p(offsets), _p(perm), _p(inv_perm), _p(y_slots), _p(y_shared),
+        None if host_out is None else ctypes.byref(host_out), _p(resid), _p(out), _stream(stream)))
 
 
 def moe_exact_residual_host(cfg, T, x_host, topk_idx_host, topk_w_host, slot_class_host,
