@@ -10,14 +10,19 @@ headline, batches 1 and 8 are reported alongside.  Weights and inputs are
 seeded synthetic draws.
 
 One step = one whole layer call on one batch: routing + bucketing, grouped FFN of
-the resident hits + shared block + LoRE corrections on the GPU, the exact-miss
-residual on the host CPU (overlapped with the GPU work), and the combine.
+the resident hits + shared block + LoRE corrections on the GPU (moe_layer_gpu), the
+exact-miss residual on the host CPU (overlapped with the GPU work), and the combine.
 Steps rotate over several independent layer instances so that the weights
 (about 0.6 GB per instance) stream from HBM and not from the 256 MB MALL.
 
-Prints one JSON line.  ``roofline`` is for the dominant kernel, the grouped FFN
-launch, timed with HIP events on its stream; ``cpu_baseline`` is the plain fp64
-oracle on a bounded sample of the same workload, on one host core.
+Prints one JSON line.  ``value`` is the end-to-end rate of whole layer calls.
+``roofline`` is for the layer's GPU path (one moe_layer_gpu call with the combine, the
+host residual precomputed): the median of back-to-back calls timed with HIP events on the
+launch stream, plain launches (graph replays alongside), against HBM; ``ffn_call`` is the
+grouped-FFN call on its own.  ``cpu_baseline`` is the plain fp64 oracle on one host core,
+``cpu_baseline_library`` the library's host path on every host core, each on a bounded
+sample of the same workload.  ``qwen2`` holds the Qwen2-57B-A14B-shaped decode batch at
+three residencies and the 4096-token prefill.
 """
 from __future__ import annotations
 
@@ -88,6 +93,8 @@ def parse():
                    help="exact-miss split (Eq. 12): auto = calibrate the cost model on this host and let the "
                         "planner fetch experts to the GPU when that beats all-CPU; off = all-CPU")
     p.add_argument("--fetch-slots", type=int, default=8, help="fetch pool slots for the exact-miss split")
+    p.add_argument("--gpu-reps", type=int, default=100, help="calls timed for the GPU path (median)")
+    p.add_argument("--no-qwen2", action="store_true", help="skip the Qwen2-57B-A14B-shaped decode/prefill records")
     p.add_argument("--weights", default="bf16", choices=("bf16", "mxfp4"),
                    help="dsv2_decode: routed experts' weights in bf16 (default) or MXFP4 (E2M1 + an E8M0 scale "
                         "per 32; the exact-miss split then stays off)")
@@ -121,25 +128,94 @@ def expert_bytes(wl) -> int:
 
 
 def algorithmic_bytes(shape, idx, cls, e_bytes=None):
-    """Bytes the method must move on the GPU for one layer call, by kernel.
-
-    ffn: distinct HIT experts x expert bytes + shared block + distinct LoRE experts x
-         factor bytes + x read + y rows written (HIT/LoRE slots fp32, shared fp32).
-    route: router weight + x.  combine: y rows + shared + resid read, out written."""
+    """Bytes the method must move on the GPU for one layer call (the survey's definition):
+    router + shared block + distinct HIT experts x expert bytes + distinct LoRE experts x
+    factor bytes + x read + out written.  Skipped non-resident experts and the fp32 scratch
+    rows (y_slots, y_shared, H) are not counted.  ffn: the share of the grouped-FFN call
+    (shared block, HIT experts, LoRE factors, x)."""
     T, K = idx.shape
     d, wb = shape.d, shape.wbytes
     hit_e = len(set(idx[cls == 0].tolist()))
     lore_e = len(set(idx[cls == 1].tolist()))
-    n_hit, n_lore = int((cls == 0).sum()), int((cls == 1).sum())
     x_b = T * d * wb
     eb = shape.expert_bytes if e_bytes is None else e_bytes
-    ffn = (hit_e * eb + shape.shared_bytes + lore_e * shape.lore_bytes + x_b
-           + (n_hit + n_lore) * d * 4 + T * d * 4)
-    route = shape.n_experts * d * wb + x_b
-    combine = (n_hit + n_lore) * d * 4 + 2 * T * d * 4 + T * d * wb
-    return dict(ffn=ffn, route=route, combine=combine, total=ffn + route + combine, hit_experts=hit_e,
-                lore_experts=lore_e, slots=np.bincount(cls.ravel(), minlength=3).tolist(),
-                exact_experts=len(set(idx[cls == 2].tolist())))
+    ffn = hit_e * eb + shape.shared_bytes + lore_e * shape.lore_bytes + x_b
+    total = shape.n_experts * d * wb + ffn + T * d * wb
+    return dict(ffn=ffn, total=total, hit_experts=hit_e, lore_experts=lore_e,
+                slots=np.bincount(cls.ravel(), minlength=3).tolist(), exact_experts=len(set(idx[cls == 2].tolist())))
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def time_gpu_path(devs, xs, confs, runs, T, reps: int = 100, warm: int = 10, graphs: bool = True):
+    """The GPU path of a layer call (moe_layer_gpu with the combine; routing, FFN, LoRE and
+    combine, the host copies included, the exact residual precomputed in each run's pinned
+    buffer), back to back over the layer instances: median us per call from HIP events on
+    the launch stream, with plain launches and as replays of one captured HIP graph per
+    instance.  A spin kernel queued first lets the host queue every call before the GPU
+    reaches it, so no event span holds host submission time."""
+    import torch
+
+    n = len(devs)
+
+    def call(i):
+        runs[i].layer_gpu(devs[i], xs[i], confs[i], T, to_host=True, resid=runs[i].resid, out=True, mark=False)
+
+    for w in range(warm):
+        call(w % n)
+    torch.cuda.synchronize()
+    ref_out = []
+    for i in range(n):
+        call(i)
+        torch.cuda.synchronize()
+        ref_out.append(runs[i].out[:T].clone())
+
+    def timed(fn):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        torch.cuda.synchronize()
+        torch.cuda._sleep(int(2e7))
+        for k in range(reps):
+            evs[k][0].record()
+            fn(k % n)
+            evs[k][1].record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+
+    plain = timed(call)
+    graph_us, graph_ok = None, None
+    if graphs:
+        try:
+            gs = []
+            side = torch.cuda.Stream()
+            for i in range(n):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=side):
+                    call(i)
+                gs.append(g)
+            torch.cuda.synchronize()
+            graph_us = timed(lambda i: gs[i].replay())
+            # every replay's output equals the eager call's (eager work and a sync in between)
+            graph_ok = True
+            for i in range(n):
+                call(i)
+                torch.cuda.synchronize()
+                gs[i].replay()
+                torch.cuda.synchronize()
+                graph_ok &= bool(torch.equal(runs[i].out[:T], ref_out[i]))
+        except Exception as ex:  # capture not available: report plain launches only
+            print(f"[bench] graph capture failed: {ex}", file=sys.stderr, flush=True)
+            graph_us, graph_ok = None, None
+    if any(r.flags() != 0 for r in runs):
+        raise RuntimeError("device flags raised during the GPU-path timing")
+    return plain, graph_us, graph_ok
 
 
 def main():
@@ -181,13 +257,16 @@ def main():
                           wfmt=wl.wfmt)
         xs = [LY.to_tensor(synth.gen_x(wl, i, 0, T), shape.dtype, "cuda") for i in range(args.instances)]
         confs = [torch.from_numpy(synth.gen_conf(wl, i, 0, T)).cuda() for i in range(args.instances)]
-        # per-instance class counts (fixed inputs per instance) from one untimed call
-        per_inst = []
+        # per instance: one untimed layer call, for the class counts (fixed inputs per instance)
+        # and the exact residual that the GPU-path timing takes as precomputed
+        per_inst, gruns = [], []
         for i in range(args.instances):
-            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
+            r = LY.LayerRun(shape, T, devs[i].C, tau=wl.tau, wfmt=wl.wfmt)
+            r.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
             torch.cuda.synchronize()
-            per_inst.append(algorithmic_bytes(shape, run.idx_host[:T].numpy().copy(),
-                                              run.cls_host[:T].numpy().copy(), expert_bytes(wl)))
+            per_inst.append(algorithmic_bytes(shape, r.idx_host[:T].numpy().copy(), r.cls_host[:T].numpy().copy(),
+                                              expert_bytes(wl)))
+            gruns.append(r)
         for w in range(args.warmup):
             i = w % args.instances
             run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads)
@@ -206,59 +285,47 @@ def main():
                 i = w % args.instances
                 run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, split=split)
             torch.cuda.synchronize()
-        fetched, host_t, host_e = [], [], []
 
-        names = ("start", "routed", "ffn0", "experts", "resid", "end")
-        evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
-        host_s = 0.0
+        # end to end: whole layer calls, the host's exact residual overlapped with the GPU
+        fetched, host_t, host_e = [], [], []
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for k in range(args.steps):
             i = k % args.instances
-            h0 = time.perf_counter()
-            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, events=evs[k], split=split)
-            host_s += time.perf_counter() - h0
+            run.forward(devs[i], xs[i], confs[i], T, n_threads=args.threads, split=split)
             fetched.append(len(run.last_fetch))
             host_t.append(run.last_host_s)
             host_e.append(run.last_host_experts)
         torch.cuda.synchronize()
         wall = time.perf_counter() - t0
+        if run.flags() != 0:
+            raise RuntimeError("device flags raised during the timed steps")
 
-        ffn_ms = np.array([e["ffn0"].elapsed_time(e["experts"]) for e in evs])
-        route_ms = np.array([e["start"].elapsed_time(e["routed"]) for e in evs])
-        comb_ms = np.array([e["resid"].elapsed_time(e["end"]) for e in evs])
-        wait_ms = np.array([e["experts"].elapsed_time(e["resid"]) for e in evs])
-        inst = [k % args.instances for k in range(args.steps)]
-        ffn_bytes = np.array([per_inst[i]["ffn"] for i in inst], dtype=np.float64)
-        tot_bytes = np.array([per_inst[i]["total"] for i in inst], dtype=np.float64)
-        gpu_ms = route_ms + ffn_ms + comb_ms
+        # the GPU path alone (the survey's t_gpu)
+        gpu_us, graph_us, graph_ok = time_gpu_path(devs, xs, confs, gruns, T, reps=args.gpu_reps)
+        tot_bytes = float(np.mean([p["total"] for p in per_inst]))
         results[T] = dict(
-            T=T, wall_s=wall, ms_per_step=1e3 * wall / args.steps,
-            tokens_per_s=T * args.steps / wall,
-            gpu_ms_per_step=float(gpu_ms.mean()),
-            gpu_tokens_per_s=float(T / (gpu_ms.mean() * 1e-3)),
-            gpu_GBps=float(tot_bytes.sum() / (gpu_ms.sum() * 1e-3) / 1e9),
-            route_us=float(route_ms.mean() * 1e3), ffn_us=float(ffn_ms.mean() * 1e3),
-            combine_us=float(comb_ms.mean() * 1e3), wait_for_host_us=float(wait_ms.mean() * 1e3),
-            ffn_GBps=float(ffn_bytes.sum() / (ffn_ms.sum() * 1e-3) / 1e9),
-            ffn_bytes_per_launch=float(ffn_bytes.mean()),
-            fetched_experts_per_step=float(np.mean(fetched)),
+            T=T, wall_s=wall, ms_per_step=1e3 * wall / args.steps, tokens_per_s=T * args.steps / wall,
+            gpu_us=gpu_us, gpu_tokens_per_s=T / (gpu_us * 1e-6), gpu_GBps=tot_bytes / (gpu_us * 1e-6) / 1e9,
+            gpu_graph_us=graph_us, graph_matches_eager=graph_ok,
+            gpu_graph_GBps=(tot_bytes / (graph_us * 1e-6) / 1e9) if graph_us else None,
+            bytes_per_call=tot_bytes, fetched_experts_per_step=float(np.mean(fetched)),
             host_exact_ms=float(np.mean(host_t) * 1e3), host_exact_experts=float(np.mean(host_e)),
             host_exact_GBps=float(np.sum(host_e) * expert_bytes(wl) / max(np.sum(host_t), 1e-12) / 1e9),
             classes=per_inst[0]["slots"], hit_experts=[p["hit_experts"] for p in per_inst],
             lore_experts=[p["lore_experts"] for p in per_inst], exact_experts=[p["exact_experts"] for p in per_inst],
         )
-        # the grouped-FFN launch on its own: back-to-back calls rotating over the instances,
-        # each bracketed by events on the launch stream (inside the step the events also
-        # catch the host's submission latency after the route kernel)
+        # the grouped-FFN call on its own (moe_expert_ffn_grouped, LoRE fused)
         launch_us, launch_bytes = time_ffn_launches(devs, xs, confs, per_inst, shape, wl, T, args)
-        results[T].update(ffn_launch_us=launch_us, ffn_launch_GBps=launch_bytes / (launch_us * 1e-6) / 1e9,
-                          ffn_launch_bytes=launch_bytes)
+        results[T].update(ffn_call_us=launch_us, ffn_call_GBps=launch_bytes / (launch_us * 1e-6) / 1e9,
+                          ffn_call_bytes=launch_bytes)
         print(f"[bench] T={T}: {json.dumps(results[T])}", file=sys.stderr, flush=True)
-        del run
+        del run, gruns
 
     head = results[batches[-1]]
     mx = args.weights == "mxfp4"
+    kern = ("layer_route_kernel + layer_up_kernel + layer_down_kernel + combine_kernel" if not mx else
+            "route_logits_kernel + route_bucket_kernel + ffn_up_mx_kernel + ffn_down_mx_kernel + combine_kernel")
     line = {
         "metric": METRIC, "value": round(head["tokens_per_s"], 1), "unit": "tokens/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(head["ms_per_step"], 4),
@@ -270,18 +337,25 @@ def main():
                    "shared_inter": shape.shared_inter, "lore_rank": shape.lore_rank, "resident": wl.resident,
                    "tau": wl.tau, "tokens": head["T"], "layer_instances": args.instances,
                    "host_threads": args.threads or os.cpu_count()},
-        "roofline": {"bound": "hbm", "kernel": "grouped expert FFN call: " + (
+        "roofline": {"bound": "hbm",
+                     "kernel": f"the layer's GPU path, one moe_layer_gpu call with the combine: {kern}",
+                     "achieved": round(head["gpu_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(head["gpu_GBps"] / HBM_PEAK_GBS, 4),
+                     "traffic": recorded_traffic("layer_" + args.weights),
+                     "bytes_per_call": int(head["bytes_per_call"]), "median_us": round(head["gpu_us"], 2),
+                     "graph_median_us": round(head["gpu_graph_us"], 2) if head["gpu_graph_us"] else None,
+                     "graph_frac": round(head["gpu_graph_GBps"] / HBM_PEAK_GBS, 4) if head["gpu_graph_GBps"] else None,
+                     "by_batch": {str(T): {"us": round(r["gpu_us"], 2), "frac": round(r["gpu_GBps"] / HBM_PEAK_GBS, 4),
+                                           "graph_us": round(r["gpu_graph_us"], 2) if r["gpu_graph_us"] else None,
+                                           "tokens_per_s": round(r["gpu_tokens_per_s"], 1),
+                                           "bytes_per_call": int(r["bytes_per_call"])}
+                                  for T, r in results.items()}},
+        "ffn_call": {"kernel": "grouped expert FFN call alone: " + (
                          "ffn_up_mx_kernel + ffn_down_mx_kernel" if mx else "ffn_up_kernel + ffn_down_kernel") +
-                     " (moe_expert_ffn_grouped with LoRE fused)",
-                     "achieved": round(head["ffn_launch_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(head["ffn_launch_GBps"] / HBM_PEAK_GBS, 4),
-                     "traffic": recorded_traffic(args.weights),
-                     "bytes_per_launch": int(head["ffn_launch_bytes"]), "avg_launch_us": round(head["ffn_launch_us"], 2),
-                     "in_step_us": round(head["ffn_us"], 2)},
-        "gpu_path": {"tokens_per_s": round(head["gpu_tokens_per_s"], 1), "ms_per_step": round(head["gpu_ms_per_step"], 4),
-                     "GBps": round(head["gpu_GBps"], 1), "frac_hbm_peak": round(head["gpu_GBps"] / HBM_PEAK_GBS, 4),
-                     "route_us": round(head["route_us"], 2), "ffn_us": round(head["ffn_us"], 2),
-                     "combine_us": round(head["combine_us"], 2)},
+                     " (moe_expert_ffn_grouped, LoRE fused)",
+                     "achieved": round(head["ffn_call_GBps"], 1), "frac": round(head["ffn_call_GBps"] / HBM_PEAK_GBS, 4),
+                     "avg_launch_us": round(head["ffn_call_us"], 2), "bytes_per_call": int(head["ffn_call_bytes"]),
+                     "traffic": recorded_traffic(args.weights)},
         "host_path": {"exact_ms": round(head["host_exact_ms"], 3), "experts_per_step": round(head["host_exact_experts"], 2),
                       "GBps": round(head["host_exact_GBps"], 1),
                       "note": "exact-miss residual on the host CPU (Eq. 12 M_cpu): bound by host DRAM reads"},
@@ -291,7 +365,13 @@ def main():
                         "cost_model_by_batch": {str(T): c for T, c in split_info.items()}},
     }
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl.with_(tokens=head["T"]), hosts[0], args.cpu_baseline_seconds)
+        wl_h = wl.with_(tokens=head["T"])
+        line["cpu_baseline"] = cpu_baseline(wl_h, hosts[0], args.cpu_baseline_seconds)
+        line["cpu_baseline_library"] = cpu_library_baseline(wl_h, hosts[0], devs[0], args.cpu_baseline_seconds / 3)
+    del devs, hosts
+    torch.cuda.empty_cache()
+    if not args.no_qwen2 and not mx:
+        line["qwen2"] = qwen2_records(args)
     if args.calib_copy_mib > 0:
         a = torch.empty(args.calib_copy_mib << 20, dtype=torch.uint8, device="cuda")
         torch.empty_like(a).copy_(a)
@@ -620,8 +700,136 @@ def cpu_baseline(wl, host, budget_s):
         steps += 1
     el = time.perf_counter() - t0
     return {"value": round(tokens / el, 3), "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "cpu_model": cpu_model(), "nproc": os.cpu_count(),
             "sample": f"{tokens} tokens ({steps} batch(es) of {wl.tokens}) of one DSV2-Lite layer: routing for the "
                       f"whole batch + full fp64 layer output per token, {el:.1f}s"}
+
+
+def cpu_library_baseline(wl, host, dev, budget_s):
+    """The library's host path as a whole-layer CPU implementation: every slot of a batch
+    treated as an exact miss (moe_exact_residual_host over all routed experts) plus the
+    shared block (the same entry with the shared block as a one-expert layer), on all host
+    threads.  Routing comes from the oracle, outside the timed calls."""
+    import oracle as orc
+    from paper_2608_21240_amd import spice, synth, workloads as W
+
+    s, T = wl.shape, wl.tokens
+    cfg = spice.make_cfg(s, 0, tau=wl.tau)
+    sh = W.MoEShape(s.d, 1, 1, s.shared_inter, 0, 0, s.dtype)
+    cfg_sh = spice.make_cfg(sh, 0)
+    ocfg = orc.make_cfg(s, tau=wl.tau)
+    w13 = [host.expert(e)[0] for e in range(s.n_experts)]
+    w2 = [host.expert(e)[1] for e in range(s.n_experts)]
+    resid = np.zeros((T, s.d), np.float32)
+    resid_s = np.zeros((T, s.d), np.float32)
+    zero_idx = np.zeros((T, 1), np.int32)
+    one_w = np.ones((T, 1), np.float32)
+    exact1 = np.full((T, 1), 2, np.uint8)
+    nproc = os.cpu_count() or 1
+    spent, tokens, steps = 0.0, 0, 0
+    while spent < budget_s or steps < 2:
+        x = synth.gen_x(wl, 0, 2000 + steps, T)
+        r = orc.route(ocfg, x, host.wg, host.bias, host.resident_mask(), synth.gen_conf(wl, 0, 2000 + steps, T))
+        idx = np.ascontiguousarray(r["idx"], np.int32)
+        g = np.ascontiguousarray(r["g"], np.float32)
+        cls = np.full(idx.shape, 2, np.uint8)
+        t0 = time.perf_counter()
+        spice.moe_exact_residual_host(cfg, T, x, idx, g, cls, w13, w2, resid, nproc)
+        spice.moe_exact_residual_host(cfg_sh, T, x, zero_idx, one_w, exact1, [host.w13s], [host.w2s], resid_s, nproc)
+        el = time.perf_counter() - t0
+        if steps > 0:  # the first call warms the host caches and the worker pool
+            spent += el
+            tokens += T
+        steps += 1
+    wbytes = s.n_experts * s.expert_bytes + s.shared_bytes
+    return {"value": round(tokens / spent, 1), "unit": "tokens/s", "cores": nproc, "kind": "library host path",
+            "cpu_model": cpu_model(),
+            "sample": f"{tokens} tokens ({steps - 1} timed batches of {T}) of one DSV2-Lite layer: every slot exact "
+                      f"(moe_exact_residual_host) plus the shared block, {nproc} threads, {spent:.2f}s; "
+                      f"{wbytes / 1e9:.2f} GB of host weights per batch at most"}
+
+
+def qwen2_records(args):
+    """The Qwen2-57B-A14B-shaped layer (Sec. 5.1's second model): the 16-token decode batch at
+    16, 32 and 48 resident experts (Zipf(1.1) skew, logit bias ln p) timed as the GPU path of
+    a layer call (moe_layer_gpu with the combine; a pinned zero residual stands in for the
+    host's, which is not computed here), against HBM; and the 4096-token prefill with all 64
+    resident, its grouped-FFN call against the bf16 MFMA peak."""
+    import torch
+
+    from paper_2608_21240_amd import layer as LY, synth, workloads as W
+
+    wl = W.WORKLOADS["qwen2_prefill"]
+    s = wl.shape
+    t0 = time.time()
+    host = LY.HostLayer(wl, 0)
+    dev = LY.DeviceLayer(host, host_exact=False)
+    torch.cuda.synchronize()
+    print(f"[bench] qwen2 layer ready in {time.time() - t0:.1f}s ({dev.hbm_bytes() / 1e9:.2f} GB HBM)",
+          file=sys.stderr, flush=True)
+    slot_all = dev.resident_slot.clone()
+    out = {"model": "Qwen2-57B-A14B-shaped layer (d 3584, 64 experts, top-8, I 2560, shared I 20480, LoRE rank 64)"}
+    dec = {}
+    T = 16
+    for R in (16, 32, 48):
+        wlr = W.WORKLOADS[f"qwen2_decode_r{R}"]
+        res = synth.resident_experts(wlr, 0)
+        rs = torch.full_like(slot_all, -1)
+        rs[res] = slot_all[res]
+        dev.resident_slot.copy_(rs)
+        run = LY.LayerRun(s, T, dev.C, tau=wlr.tau)
+        run.resid.zero_()
+        x = LY.to_tensor(synth.gen_x(wlr, 0, 0, T), s.dtype, "cuda")
+        conf = torch.from_numpy(synth.gen_conf(wlr, 0, 0, T)).cuda()
+        run.layer_gpu(dev, x, conf, T, to_host=False, resid=run.resid, out=True)
+        torch.cuda.synchronize()
+        idx, cls = run.topk_idx.cpu().numpy(), run.slot_class.cpu().numpy()
+        b = algorithmic_bytes(s, idx, cls)
+        us, gus, gok = time_gpu_path([dev], [x], [conf], [run], T, reps=max(20, args.gpu_reps // 3))
+        dec[f"R{R}"] = {"resident": R, "tokens": T, "median_us": round(us, 2), "tokens_per_s": round(T / (us * 1e-6), 1),
+                        "bytes_per_call": int(b["total"]), "GBps": round(b["total"] / (us * 1e-6) / 1e9, 1),
+                        "frac": round(b["total"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                        "graph_us": round(gus, 2) if gus else None, "graph_matches_eager": gok,
+                        "slots": b["slots"], "hit_experts": b["hit_experts"], "lore_experts": b["lore_experts"]}
+        print(f"[bench] qwen2 decode R={R}: {json.dumps(dec[f'R{R}'])}", file=sys.stderr, flush=True)
+        del run
+    dev.resident_slot.copy_(slot_all)
+    out["decode_T16"] = dec
+    # prefill: all 64 resident, every slot a HIT
+    T = wl.tokens
+    run = LY.LayerRun(s, T, dev.C, tau=wl.tau)
+    x = LY.to_tensor(synth.gen_x(wl, 0, 0, T), s.dtype, "cuda")
+    conf = torch.from_numpy(synth.gen_conf(wl, 0, 0, T)).cuda()
+    run.layer_gpu(dev, x, conf, T, to_host=False, resid=None, out=True)
+    torch.cuda.synchronize()
+    cls = run.slot_class.cpu().numpy()
+    n_hit, n_lore = int((cls == 0).sum()), int((cls == 1).sum())
+    flops = 6.0 * T * s.d * s.shared_inter + 6.0 * n_hit * s.d * s.inter + 4.0 * n_lore * s.d * s.lore_rank
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True),
+            torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(6)]
+    for a, b, c, d in evs:
+        a.record()
+        run.route(dev, x, conf, T, to_host=False)
+        b.record()
+        run.experts(dev, x, T)
+        c.record()
+        run.combine(None, T)
+        d.record()
+    torch.cuda.synchronize()
+    layer_ms = float(np.median([a.elapsed_time(d) for a, b, c, d in evs]))
+    ffn_ms = float(np.median([b.elapsed_time(c) for a, b, c, d in evs]))
+    route_ms = float(np.median([a.elapsed_time(b) for a, b, c, d in evs]))
+    out["prefill_T4096"] = {
+        "tokens": T, "resident": 64, "layer_ms": round(layer_ms, 3), "tokens_per_s": round(T / (layer_ms * 1e-3), 1),
+        "route_us": round(route_ms * 1e3, 1), "ffn_ms": round(ffn_ms, 3), "flop_per_ffn_call": flops,
+        "roofline": {"bound": "mfma", "kernel": "grouped expert FFN call: expert_gemm_kernel up + down",
+                     "achieved": round(flops / (ffn_ms * 1e-3) / 1e12, 1), "peak": MFMA_BF16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(flops / (ffn_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4)},
+        "classes": np.bincount(cls.ravel(), minlength=3).tolist()}
+    print(f"[bench] qwen2 prefill: {json.dumps(out['prefill_T4096'])}", file=sys.stderr, flush=True)
+    if run.flags() != 0:
+        raise RuntimeError("device flags raised in the Qwen2 records")
+    return out
 
 
 if __name__ == "__main__":

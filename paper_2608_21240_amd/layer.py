@@ -236,10 +236,11 @@ class LayerRun:
         self.wait_ready = False
 
     def layer_gpu(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
-                  to_host: bool = True, fuse_lore: bool = True, resid=None, out: bool = False):
+                  to_host: bool = True, fuse_lore: bool = True, resid=None, out: bool = False, mark: bool = True):
         """Routing, bucketing and the expert FFN (+ LoRE) as one library call (moe_layer_gpu);
         with to_host the routing's host copies are followed by a new ready word; with out the
-        combine runs too, with resid (device or pinned host memory, or None)."""
+        combine runs too, with resid (device or pinned host memory, or None).  mark=False
+        records no event after the call (for graph capture)."""
         T = self.T if T is None else T
         ho = None
         if to_host:
@@ -251,7 +252,8 @@ class LayerRun:
                             L.w2s, L.w_sg, la, lb, self.logits, self.topk_idx, self.topk_w, self.slot_class,
                             self.offsets, self.perm, self.inv_perm, self.y_slots, self.y_shared, ho, resid,
                             self.out if out else None, self.ws, self.ws_bytes)
-        self.e_route.record(torch.cuda.current_stream())
+        if mark:
+            self.e_route.record(torch.cuda.current_stream())
         self.wait_ready = to_host
 
     def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
