@@ -540,12 +540,13 @@ __device__ __forceinline__ void down_pass(const char* const (&a)[NA], const char
         for (int j = 0; j < NB; ++j) red[w][rr][j][lane] = acc[rr][j];
 }
 
-// Down tile rt (kDownRows x 16 rows of W2) of one group, the kind fixed at compile time:
+// Down tile rt (R x 16 rows of W2, R = 1 or 2) of one group, the kind fixed at compile time:
 // kKindHit reads H at the bucket positions and writes y_slots there; kKindShared reads the
 // shared intermediate for tokens 0..T-1 and writes y_shared (times sgate[t] when set).
-template <int DT, int KIND>
+template <int DT, int KIND, int R = kDownRows>
 __device__ void down_tile(const FfnArgs& a, const Group& g, int rt, f32x4_t (&red)[kWaves][kDownRows][kTokTiles][64]) {
     static_assert(KIND == kKindHit || KIND == kKindShared, "down tiles are HIT or shared");
+    static_assert(R == 1 || R == kDownRows, "16 or 32 rows per down tile");
     using T_ = Tr<DT>;
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
     const int lane = threadIdx.x & 63;
@@ -572,23 +573,29 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, int rt, f32x4_t (&re
         ld = a.ldhs;
     }
     const int m = lane & 15, quad = lane >> 4;
-    const int dim0 = rt * 16 * kDownRows;
+    const int dim0 = rt * 16 * R;
     const size_t kb = (size_t)quad * T_::kLaneK * es;
     const char* const aw[kDownRows] = {
         // tail rows read the last row; their outputs are dropped
         static_cast<const char*>(wbase) + (row0 + min(dim0 + m, a.d - 1)) * (size_t)kdim * es + kb,
         static_cast<const char*>(wbase) + (row0 + min(dim0 + 16 + m, a.d - 1)) * (size_t)kdim * es + kb};
+    const char* const a1[1] = {aw[0]};
     for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
         const char* const hb[kTokTiles] = {
             static_cast<const char*>(hbase) + (size_t)(start + min(g0 + m, n - 1)) * ld * es + kb,
             static_cast<const char*>(hbase) + (size_t)(start + min(g0 + 16 + m, n - 1)) * ld * es + kb};
         const char* const h1[1] = {hb[0]};
-        if (ntt == 1) down_pass<DT, kDownRows, 1>(aw, h1, kdim, w, quad, red, lane);
-        else down_pass<DT, kDownRows, 2>(aw, hb, kdim, w, quad, red, lane);
+        if constexpr (R == 1) {
+            if (ntt == 1) down_pass<DT, 1, 1>(a1, h1, kdim, w, quad, red, lane);
+            else down_pass<DT, 1, 2>(a1, hb, kdim, w, quad, red, lane);
+        } else {
+            if (ntt == 1) down_pass<DT, kDownRows, 1>(aw, h1, kdim, w, quad, red, lane);
+            else down_pass<DT, kDownRows, 2>(aw, hb, kdim, w, quad, red, lane);
+        }
         __syncthreads();
         // wave w finalises (row tile, token tile) pair w
-        const int rr = w % kDownRows, tt = w / kDownRows;
+        const int rr = w % R, tt = w / R;
         if (tt < ntt) {
             f32x4_t s = red[0][rr][tt][lane];
 #pragma unroll

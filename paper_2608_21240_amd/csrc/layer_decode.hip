@@ -23,6 +23,9 @@
 namespace spice {
 namespace {
 
+// Largest T whose HIT down tiles take 16 rows instead of 32.
+constexpr int kDownRows16MaxT = 8;
+
 // Most slots T*K for which the up tiles bucket locally (4 per thread).
 constexpr int kLocalPer = 4;
 static_assert(kLayerMaxSlots == kLocalPer * kThreads, "local bucketing covers kLayerMaxSlots slots");
@@ -41,7 +44,7 @@ struct LayerGridB {
     int tsh_dn, nlore, tlore, nhit, thit;
 };
 struct LayerGridC {
-    int nlore, tlore, nhit, thit;
+    int nlore, tlore, nhit, thit, rows16;  // rows16: HIT down tiles of 16 rows (small T), else 32
 };
 
 __device__ __forceinline__ int wave_sum_int(int v) {
@@ -188,7 +191,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     b -= 1;
     if (b < gr.tsh_dn) {
         const Group g{0, 0, f.T, -1};
-        down_tile<DT, kKindShared>(f, g, b, *reinterpret_cast<f32x4_t(*)[kWaves][kDownRows][kTokTiles][64]>(lds));
+        down_tile<DT, kKindShared, 1>(f, g, b, *reinterpret_cast<f32x4_t(*)[kWaves][kDownRows][kTokTiles][64]>(lds));
         return;
     }
     b -= gr.tsh_dn;
@@ -222,7 +225,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     b -= gr.nlore * gr.tlore;
     if (b < gr.nhit * gr.thit) {
         if (!work_group(f, r, SPICE_CLASS_HIT, b / gr.thit, g)) return;
-        down_tile<DT, kKindHit>(f, g, b % gr.thit, red);
+        if (gr.rows16) down_tile<DT, kKindHit, 1>(f, g, b % gr.thit, red);
+        else down_tile<DT, kKindHit>(f, g, b % gr.thit, red);
     }
 }
 
@@ -233,9 +237,14 @@ hipError_t launch_layer_decode(const RouteArgs& r, const FfnArgs& f, hipStream_t
     const bool shared = f.Is > 0, lore = f.r > 0;
     const int gpt = route_blocks_per_token(r.N + (r.w_sg ? 1 : 0), kThreads);
     LayerGridA ga{f.T * gpt, gpt, shared ? (f.Is + 15) / 16 : 0};
-    LayerGridB gb{shared ? (f.d + 16 * kDownRows - 1) / (16 * kDownRows) : 0, lore ? std::min(f.N, S) : 0,
-                  (f.r + 15) / 16, f.C > 0 ? std::min(std::min(f.N, f.C), S) : 0, (f.I + 15) / 16};
-    LayerGridC gc{gb.nlore, (f.d + kLoreRows - 1) / kLoreRows, gb.nhit, (f.d + 16 * kDownRows - 1) / (16 * kDownRows)};
+    // the shared block's down tiles take 16 rows (twice as many, half as long: they would
+    // otherwise be the longest tiles of the launch at small T); so do the HIT down tiles
+    // while the batch is small (few experts, so too few tiles to fill the GPU)
+    const bool rows16 = f.T <= kDownRows16MaxT;
+    LayerGridB gb{shared ? (f.d + 15) / 16 : 0, lore ? std::min(f.N, S) : 0, (f.r + 15) / 16,
+                  f.C > 0 ? std::min(std::min(f.N, f.C), S) : 0, (f.I + 15) / 16};
+    LayerGridC gc{gb.nlore, (f.d + kLoreRows - 1) / kLoreRows, gb.nhit,
+                  rows16 ? (f.d + 15) / 16 : (f.d + 16 * kDownRows - 1) / (16 * kDownRows), rows16 ? 1 : 0};
     const unsigned na = (unsigned)(ga.nroute + ga.tsh);
     const unsigned nb = (unsigned)(1 + gb.tsh_dn + gb.nlore * gb.tlore + gb.nhit * gb.thit);
     const unsigned nc = (unsigned)(gc.nlore * gc.tlore + gc.nhit * gc.thit);
