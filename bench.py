@@ -17,8 +17,9 @@ Steps rotate over several independent layer instances so that the weights
 
 Prints one JSON line.  ``value`` is the end-to-end rate of whole layer calls.
 ``roofline`` is for the layer's GPU path (one moe_layer_gpu call with the combine, the
-host residual precomputed): the median of back-to-back calls timed with HIP events on the
-launch stream, plain launches (graph replays alongside), against HBM; ``ffn_call`` is the
+host residual precomputed): the average duration of back-to-back calls, from HIP events on
+the launch stream around the timed calls (the median of per-call event pairs and graph
+replays alongside), against HBM; ``ffn_call`` is the
 grouped-FFN call on its own.  ``cpu_baseline`` is the plain fp64 oracle on one host core,
 ``cpu_baseline_library`` the library's host path on every host core, each on a bounded
 sample of the same workload.  ``qwen2`` holds the Qwen2-57B-A14B-shaped decode batch at
@@ -158,10 +159,13 @@ def cpu_model() -> str:
 def time_gpu_path(devs, xs, confs, runs, T, reps: int = 100, warm: int = 10, graphs: bool = True):
     """The GPU path of a layer call (moe_layer_gpu with the combine; routing, FFN, LoRE and
     combine, the host copies included, the exact residual precomputed in each run's pinned
-    buffer), back to back over the layer instances: median us per call from HIP events on
-    the launch stream, with plain launches and as replays of one captured HIP graph per
-    instance.  A spin kernel queued first lets the host queue every call before the GPU
-    reaches it, so no event span holds host submission time."""
+    buffer), back to back over the layer instances, with plain launches and as replays of
+    one captured HIP graph per instance.  Two timings of each on the launch stream: the
+    mean per call over one event pair around `reps` back-to-back calls (the average
+    duration the roofline uses), and the median of per-call event pairs (a latency figure;
+    each pair adds its own markers to the stream).  A spin kernel queued first lets the
+    host queue every call before the GPU reaches it, so no span holds host submission
+    time.  Returns ((mean, median), (graph mean, graph median) or None, graph_ok)."""
     import torch
 
     n = len(devs)
@@ -179,18 +183,27 @@ def time_gpu_path(devs, xs, confs, runs, T, reps: int = 100, warm: int = 10, gra
         ref_out.append(runs[i].out[:T].clone())
 
     def timed(fn):
+        spin = int(2e7 + 2e5 * reps)
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
         torch.cuda.synchronize()
-        torch.cuda._sleep(int(2e7))
+        torch.cuda._sleep(spin)
         for k in range(reps):
             evs[k][0].record()
             fn(k % n)
             evs[k][1].record()
         torch.cuda.synchronize()
-        return float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+        median = float(np.median([a.elapsed_time(b) for a, b in evs]) * 1e3)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda._sleep(spin)
+        a.record()
+        for k in range(reps):
+            fn(k % n)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) * 1e3 / reps, median
 
     plain = timed(call)
-    graph_us, graph_ok = None, None
+    graph, graph_ok = None, None
     if graphs:
         try:
             gs = []
@@ -201,7 +214,7 @@ def time_gpu_path(devs, xs, confs, runs, T, reps: int = 100, warm: int = 10, gra
                     call(i)
                 gs.append(g)
             torch.cuda.synchronize()
-            graph_us = timed(lambda i: gs[i].replay())
+            graph = timed(lambda i: gs[i].replay())
             # every replay's output equals the eager call's (eager work and a sync in between)
             graph_ok = True
             for i in range(n):
@@ -212,10 +225,10 @@ def time_gpu_path(devs, xs, confs, runs, T, reps: int = 100, warm: int = 10, gra
                 graph_ok &= bool(torch.equal(runs[i].out[:T], ref_out[i]))
         except Exception as ex:  # capture not available: report plain launches only
             print(f"[bench] graph capture failed: {ex}", file=sys.stderr, flush=True)
-            graph_us, graph_ok = None, None
+            graph, graph_ok = None, None
     if any(r.flags() != 0 for r in runs):
         raise RuntimeError("device flags raised during the GPU-path timing")
-    return plain, graph_us, graph_ok
+    return plain, graph, graph_ok
 
 
 def main():
@@ -302,12 +315,14 @@ def main():
             raise RuntimeError("device flags raised during the timed steps")
 
         # the GPU path alone (the survey's t_gpu)
-        gpu_us, graph_us, graph_ok = time_gpu_path(devs, xs, confs, gruns, T, reps=args.gpu_reps)
+        (gpu_us, gpu_med), graph, graph_ok = time_gpu_path(devs, xs, confs, gruns, T, reps=args.gpu_reps)
+        graph_us, graph_med = graph if graph else (None, None)
         tot_bytes = float(np.mean([p["total"] for p in per_inst]))
         results[T] = dict(
             T=T, wall_s=wall, ms_per_step=1e3 * wall / args.steps, tokens_per_s=T * args.steps / wall,
-            gpu_us=gpu_us, gpu_tokens_per_s=T / (gpu_us * 1e-6), gpu_GBps=tot_bytes / (gpu_us * 1e-6) / 1e9,
-            gpu_graph_us=graph_us, graph_matches_eager=graph_ok,
+            gpu_us=gpu_us, gpu_median_us=gpu_med, gpu_tokens_per_s=T / (gpu_us * 1e-6),
+            gpu_GBps=tot_bytes / (gpu_us * 1e-6) / 1e9,
+            gpu_graph_us=graph_us, gpu_graph_median_us=graph_med, graph_matches_eager=graph_ok,
             gpu_graph_GBps=(tot_bytes / (graph_us * 1e-6) / 1e9) if graph_us else None,
             bytes_per_call=tot_bytes, fetched_experts_per_step=float(np.mean(fetched)),
             host_exact_ms=float(np.mean(host_t) * 1e3), host_exact_experts=float(np.mean(host_e)),
@@ -342,10 +357,12 @@ def main():
                      "achieved": round(head["gpu_GBps"], 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(head["gpu_GBps"] / HBM_PEAK_GBS, 4),
                      "traffic": recorded_traffic("layer_" + args.weights),
-                     "bytes_per_call": int(head["bytes_per_call"]), "median_us": round(head["gpu_us"], 2),
-                     "graph_median_us": round(head["gpu_graph_us"], 2) if head["gpu_graph_us"] else None,
+                     "bytes_per_call": int(head["bytes_per_call"]), "avg_call_us": round(head["gpu_us"], 2),
+                     "median_call_us": round(head["gpu_median_us"], 2),
+                     "graph_avg_call_us": round(head["gpu_graph_us"], 2) if head["gpu_graph_us"] else None,
                      "graph_frac": round(head["gpu_graph_GBps"] / HBM_PEAK_GBS, 4) if head["gpu_graph_GBps"] else None,
                      "by_batch": {str(T): {"us": round(r["gpu_us"], 2), "frac": round(r["gpu_GBps"] / HBM_PEAK_GBS, 4),
+                                           "median_us": round(r["gpu_median_us"], 2),
                                            "graph_us": round(r["gpu_graph_us"], 2) if r["gpu_graph_us"] else None,
                                            "tokens_per_s": round(r["gpu_tokens_per_s"], 1),
                                            "bytes_per_call": int(r["bytes_per_call"])}
@@ -785,8 +802,10 @@ def qwen2_records(args):
         torch.cuda.synchronize()
         idx, cls = run.topk_idx.cpu().numpy(), run.slot_class.cpu().numpy()
         b = algorithmic_bytes(s, idx, cls)
-        us, gus, gok = time_gpu_path([dev], [x], [conf], [run], T, reps=max(20, args.gpu_reps // 3))
-        dec[f"R{R}"] = {"resident": R, "tokens": T, "median_us": round(us, 2), "tokens_per_s": round(T / (us * 1e-6), 1),
+        (us, med), graph, gok = time_gpu_path([dev], [x], [conf], [run], T, reps=max(20, args.gpu_reps // 3))
+        gus = graph[0] if graph else None
+        dec[f"R{R}"] = {"resident": R, "tokens": T, "avg_call_us": round(us, 2), "median_call_us": round(med, 2),
+                        "tokens_per_s": round(T / (us * 1e-6), 1),
                         "bytes_per_call": int(b["total"]), "GBps": round(b["total"] / (us * 1e-6) / 1e9, 1),
                         "frac": round(b["total"] / (us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
                         "graph_us": round(gus, 2) if gus else None, "graph_matches_eager": gok,

@@ -35,6 +35,21 @@ def small_wl(shape, T, resident, **kw):
     return W.Workload("small", shape, tokens=T, resident=resident, skew=kw.pop("skew", False), **kw)
 
 
+def check_combine_in_layer_call(c):
+    """The same layer call again with the combine inside moe_layer_gpu (out given, the first
+    call's host residual as resid): the output equals the first call's (routing and FFN in
+    the layer call, then the separate combine) bit for bit."""
+    R, s, T = c.run, c.shape, c.T
+    xd = LY.to_tensor(c.x, s.dtype, "cuda")
+    conf = torch.from_numpy(np.ascontiguousarray(c.conf)).cuda()
+    out1 = R.out[:T].clone()
+    R.out.zero_()
+    R.layer_gpu(c.dev, xd, conf, T, to_host=False, resid=R.resid, out=True)
+    torch.cuda.synchronize()
+    assert R.flags() == 0
+    assert torch.equal(R.out[:T], out1), "the layer call's combine differs from the separate combine"
+
+
 @pytest.mark.parametrize("fused", [True, False])
 def test_tiny_f32_layer(fused):
     say(f"tiny_f32 fused={fused}")
@@ -58,6 +73,8 @@ def test_ragged_layers(shape, T, R, layer_call):
     c.check_outputs()
     counts = np.bincount(c.o["cls"].reshape(-1), minlength=3)
     assert (counts > 0).all(), counts  # all three classes exercised
+    if layer_call:
+        check_combine_in_layer_call(c)
 
 
 @pytest.fixture(scope="module")
@@ -78,6 +95,8 @@ def test_dsv2_decode(dsv2, T, layer_call):
     c.run_oracle()
     c.check_routing()
     c.check_outputs()
+    if layer_call:
+        check_combine_in_layer_call(c)
 
 
 @pytest.fixture(scope="module")
@@ -133,6 +152,7 @@ def test_residency_extremes(mode):
         assert (c.g["cls"] == LORE).all()
     if mode == "all_exact":
         assert (c.g["cls"] == EXACT).all()
+    check_combine_in_layer_call(c)
 
 
 @pytest.mark.parametrize("conf_mode,norm,tau", [(W.CONF_GATE, 0, 0.1), (W.CONF_GATE_RENORM, 0, 0.3),
