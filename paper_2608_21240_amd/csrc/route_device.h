@@ -67,8 +67,9 @@ __device__ __forceinline__ double route_wave_sum(double v) {
     return __shfl(v, 0);
 }
 
-// Rows per routing block: each wave owns kRouteRowsPerWave router rows of one token.
-constexpr int kRouteRowsPerWave = 4;
+// Rows per routing block: each wave owns kRouteRowsPerWave router rows of one token (one:
+// the most blocks per token, so the shortest chain to the token's last block).
+constexpr int kRouteRowsPerWave = 1;
 
 // Logits of token t for the rows [r0, r1) of the router, in fp64, by one block: row e < N is
 // W_g[e] (z = x . W_g[e] + bias[e] to logits_ws and logits_out), row N is the shared
@@ -247,6 +248,7 @@ __device__ void block_topk(const RouteArgs& a, int t, const double* zg, TopkLds&
         const int e = lane + 64 * j;
         const unsigned long long k = e < N ? L.key[e] : 0ull;
         int r = 0;
+#pragma unroll 8  // several LDS reads in flight
         for (int ee = e_lo; ee < e_hi; ++ee) {
             const unsigned long long ke = L.key[ee];
             const unsigned gt = ke > k, eq = ke == k, lt = ee < e;
