@@ -2,13 +2,19 @@
 // bucketing (Eq. 1; Sec. 2.1, 4.2, 4.3).  No block waits for another block.
 //
 // T <= kRouteTokenMaxT (decode), two launches:
-//   1. route_logits_kernel: a token's router rows are spread over a few blocks (4 rows per
-//      wave), each summing its logits in fp64; the last of the token's blocks to finish (an
-//      arrival counter per token) takes the token's top-K, gates, confidence and classes;
+//   1. route_logits_kernel: a token's router rows are spread over several blocks (one row
+//      per wave), each summing its logits in fp64; the last of the token's blocks to finish
+//      (an arrival counter per token) takes the token's top-K, gates, confidence and classes;
 //   2. route_bucket_kernel: one block sorts the T*K slots by (class, expert), writes the
 //      work lists and, when asked, the CPU path's host copies and their ready word.
-// Larger T (prefill): the logits as fp64 MFMA tiles of 16 experts x 16 tokens, a block per
-// token for the top-K, then the same bucketing block.
+// Larger T (prefill), three launches:
+//   1. route_prefill_kernel: per 16 tokens, the logits as fp64 MFMA tiles of 16 experts x
+//      16 tokens (two waves per tile, each half the contraction), then the tokens' top-K,
+//      gates and classes in the same block, and the block's histogram of bucket keys;
+//   2. bucket_scan_kernel: one block turns the histograms into each key's start (offsets,
+//      work lists, class counts) and each block's running count within every key;
+//   3. bucket_scatter_kernel: per 16 tokens, the stable positions of their slots (perm,
+//      inv_perm).  The scan block also writes the host copies when asked.
 //
 // bf16 x bf16 and fp32 x fp32 products are exact in fp64, so on every path only the
 // summation order of the logits differs from a plain loop.
@@ -19,9 +25,8 @@
 namespace spice {
 namespace {
 
-constexpr int kLogitThreads = 256;   // routing logits: 4 waves, 4 router rows each
+constexpr int kLogitThreads = 256;   // routing logits: 4 waves, kRouteRowsPerWave router rows each
 constexpr int kBucketThreads = 512;  // bucketing block
-constexpr int kMfmaThreads = 256;    // fp64 MFMA logits: 4 waves, one 16-token tile per block
 constexpr int kBucketCache = 2048;   // slots whose keys stay in LDS while bucketing (LDS <= 64 KiB at N = 256)
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
@@ -44,69 +49,330 @@ __global__ __launch_bounds__(kBucketThreads) void route_bucket_kernel(RouteArgs 
     if (a.hx || a.h_idx || a.h_w || a.h_cls || a.h_ready) mirror_host<kBucketThreads>(a);
 }
 
-// Large T: z = x W_g^T (+ bias) with v_mfma_f64_16x16x4f64.  Block = 16 tokens; wave w
-// takes the 16-expert tiles w, w + 4, ...  A 16-byte load gives each lane 8 (bf16) or 4
-// (fp32) consecutive k of one row: lane (m = lane % 16, q = lane / 16) holds row m's
-// elements q*V .. q*V + V-1 of a 4V-wide k chunk, and MFMA step u takes element u of
-// every lane, so the 4 k of step u are {u, V + u, 2V + u, 3V + u} for both operands and
-// each chunk's products are all summed once.  Rows beyond N and tokens beyond T load
-// zero and their outputs are dropped; d is a multiple of V (the ABI's alignment).
+constexpr int kPrefillThreads = 512;  // 8 waves
+constexpr int kPrefillTok = 16;       // tokens per prefill routing block (one MFMA tile wide)
+constexpr int kScanThreads = 1024;    // bucket_scan_kernel: one thread per bucket key (3N <= 768)
+static_assert(3 * SPICE_MAX_EXPERTS <= kScanThreads, "a scan thread per bucket key");
+
+// The prefill histogram table in the workspace's logits region (unused on this path: the
+// top-K reads the logits from LDS): [3N][stride] counts (key-major, one column per routing
+// block), then the [3N] key starts.
+__host__ __device__ inline int prefill_hist_stride(int T) { return ((T + kPrefillTok - 1) / kPrefillTok + 3) & ~3; }
+
+struct PrefillLds {
+    // partial logits of the contraction parts: [parts][16 tokens][N], parts x N <= 8 x 64
+    double zp[kPrefillThreads / 64 * kPrefillTok * 64];
+    double z[kPrefillTok][SPICE_MAX_EXPERTS];  // logits
+    unsigned long long key[kPrefillTok][SPICE_MAX_EXPERTS];  // their order-preserving keys
+    int res[SPICE_MAX_EXPERTS];
+    int pick[kPrefillTok][64];
+    int hist[3 * SPICE_MAX_EXPERTS];
+};
+
+// The products of up to 4 expert tiles (16 experts each, from tile0) with 16 tokens over
+// the contraction passes [p0, p1), with v_mfma_f64_16x16x4f64; each pass's x chunk is
+// widened once for all the tiles.  A 16-byte load gives each lane 8 (bf16) or 4 (fp32)
+// consecutive k of one row: lane (m = lane % 16, q = lane / 16) holds row m's elements
+// q*V .. q*V + V-1 of a 4V-wide k chunk, and MFMA step u takes element u of every lane, so
+// the 4 k of step u are {u, V + u, 2V + u, 3V + u} for both operands and each chunk's
+// products are all summed once.  A pass is two chunks; the next pass's loads are in flight
+// while one multiplies.  Rows beyond N and tokens beyond T load zero; d is a multiple of V.
 template <int DT>
-__global__ __launch_bounds__(kMfmaThreads) void route_logits_mfma_kernel(RouteArgs a) {
+__device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr, bool tok_ok, int tile0, int ntg,
+                                              int p0, int p1, int lane, f64x4_t (&out)[4]) {
     using E = RouteElem<DT>;
     constexpr int V = E::V, es = E::es;
-    const int lane = threadIdx.x & 63, m = lane & 15, q = lane >> 4;
-    const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int t0 = blockIdx.x * 16;
-    const int tok = t0 + m;
-    const bool tok_ok = tok < a.T;
-    const char* xr = static_cast<const char*>(a.x) + (size_t)(tok_ok ? tok : 0) * a.d * es;
-    const int ntile = (a.N + 15) / 16;
-    for (int tile = w; tile < ntile; tile += kMfmaThreads / 64) {
-        const int e = tile * 16 + m;
-        const bool e_ok = e < a.N;
-        const char* wr = static_cast<const char*>(a.wg) + (size_t)(e_ok ? e : 0) * a.d * es;
-        f64x4_t acc0 = {0.0, 0.0, 0.0, 0.0}, acc1 = {0.0, 0.0, 0.0, 0.0};
-        for (int k0 = 0; k0 < a.d; k0 += 8 * V) {  // two 4V-wide chunks per pass
-            uint4 xq[2], wq[2];
+    const int m = lane & 15, q = lane >> 4;
+    const char* wr[4];
+    bool e_ok[4];
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                const int k = k0 + c * 4 * V + q * V;
-                const bool in = k < a.d;
-                const size_t kk = (size_t)(in ? k : 0) * es;  // out-of-range chunks load chunk 0 as zeros
-                xq[c] = load16_or_zero(xr + kk, in && tok_ok);
-                wq[c] = load16_or_zero(wr + kk, in && e_ok);
-            }
+    for (int i = 0; i < 4; ++i) {
+        const int e = (tile0 + i) * 16 + m;
+        e_ok[i] = i < ntg && e < a.N;
+        wr[i] = static_cast<const char*>(a.wg) + (size_t)(e_ok[i] ? e : 0) * a.d * es;
+    }
+    f64x4_t acc[4][2] = {};
+    auto load = [&](int p, uint4 (&xb)[2], uint4 (&wb)[4][2]) {
 #pragma unroll
-            for (int c = 0; c < 2; ++c) {
-                double xd[V], wd[V];
-                E::widen(xq[c], xd);
-                E::widen(wq[c], wd);
+        for (int c = 0; c < 2; ++c) {
+            const int k = p * 8 * V + c * 4 * V + q * V;
+            const bool in = k < a.d;
+            const size_t kk = (size_t)(in ? k : 0) * es;  // out-of-range chunks load chunk 0 as zeros
+            xb[c] = load16_or_zero(xr + kk, in && tok_ok);
 #pragma unroll
-                for (int u = 0; u < V; u += 2) {  // two accumulators: no MFMA waits on the one before
-                    acc0 = __builtin_amdgcn_mfma_f64_16x16x4f64(wd[u], xd[u], acc0, 0, 0, 0);
-                    acc1 = __builtin_amdgcn_mfma_f64_16x16x4f64(wd[u + 1], xd[u + 1], acc1, 0, 0, 0);
+            for (int i = 0; i < 4; ++i) wb[i][c] = load16_or_zero(wr[i] + kk, in && e_ok[i]);
+        }
+    };
+    auto mul = [&](const uint4 (&xb)[2], const uint4 (&wb)[4][2]) {
+#pragma unroll
+        for (int c = 0; c < 2; ++c) {
+            double xd[V];
+            E::widen(xb[c], xd);
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                if (i < ntg) {  // uniform
+                    double wd[V];
+                    E::widen(wb[i][c], wd);
+#pragma unroll
+                    for (int u = 0; u < V; ++u)  // two accumulators per tile
+                        acc[i][u & 1] = __builtin_amdgcn_mfma_f64_16x16x4f64(wd[u], xd[u], acc[i][u & 1], 0, 0, 0);
                 }
             }
         }
-        // the f64 16x16x4 result layout: acc[v] = D[row 4v + q][column m], i.e. the logit of
-        // expert tile*16 + 4v + q for token t0 + m (a probe of the instruction fixed this)
+    };
+    if (p0 < p1) {
+        uint4 xa[2], wa[4][2], xb[2], wb[4][2];
+        load(p0, xa, wa);
+        int p = p0;
+        for (; p + 1 < p1; p += 2) {
+            load(p + 1, xb, wb);
+            mul(xa, wa);
+            load(min(p + 2, p1 - 1), xa, wa);  // past the end: reloads the last pass, unused
+            mul(xb, wb);
+        }
+        if (p < p1) mul(xa, wa);
+    }
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int ee = tile * 16 + 4 * v + q;
-            if (ee < a.N && tok_ok) {
-                const double z = (acc0[v] + acc1[v]) + (a.bias ? (double)a.bias[ee] : 0.0);
-                a.logits_ws[(size_t)tok * a.N + ee] = z;
-                if (a.logits_out) a.logits_out[(size_t)tok * a.N + ee] = z;
+    for (int i = 0; i < 4; ++i) out[i] = acc[i][0] + acc[i][1];
+}
+
+// Prefill routing of tokens [16 b, 16 b + 16): logits, top-K, gates, classes, and the
+// block's histogram of bucket keys (column b of the table).
+template <int DT>
+__global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArgs a) {
+    __shared__ PrefillLds L;
+    constexpr int kNW = kPrefillThreads / 64;
+    const int tid = threadIdx.x, lane = tid & 63, m = lane & 15, q = lane >> 4;
+    const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int N = a.N, K = a.K, NK = 3 * N;
+    const int t0 = blockIdx.x * kPrefillTok;
+    const int tok = t0 + m;
+    const bool tok_ok = tok < a.T;
+    const int es = RouteElem<DT>::es;
+    const char* xr = static_cast<const char*>(a.x) + (size_t)(tok_ok ? tok : 0) * a.d * es;
+    for (int e = tid; e < N; e += kPrefillThreads) L.res[e] = a.resident_slot[e];
+    for (int k = tid; k < NK; k += kPrefillThreads) L.hist[k] = 0;
+
+    // logits: the expert tiles in groups of 4; wave w takes group w / parts and contraction
+    // part w % parts (parts = 8 / groups), leaving its partial logits in LDS; then the parts
+    // are summed in order
+    const int ntile = (N + 15) / 16, ngroups = (ntile + 3) / 4, parts = kNW / ngroups;
+    const int npass = (a.d + 8 * RouteElem<DT>::V - 1) / (8 * RouteElem<DT>::V);
+    if (w < ngroups * parts) {
+        const int g = w / parts, kp = w - g * parts;
+        const int ntg = min(4, ntile - 4 * g);
+        f64x4_t part[4];
+        prefill_group<DT>(a, xr, tok_ok, 4 * g, ntg, kp * npass / parts, (kp + 1) * npass / parts, lane, part);
+        // result layout of the f64 16x16x4 product: element v of lane (m, q) is expert
+        // tile*16 + 4v + q for token t0 + m
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int ee = (4 * g + i) * 16 + 4 * v + q;
+                if (i < ntg && ee < N) L.zp[(kp * kPrefillTok + m) * N + ee] = part[i][v];
+            }
+    }
+    __syncthreads();
+    for (int i = tid; i < kPrefillTok * N; i += kPrefillThreads) {
+        const int tt = i / N, ee = i - tt * N;
+        double z = L.zp[tt * N + ee];
+        for (int kp = 1; kp < parts; ++kp) z += L.zp[(kp * kPrefillTok + tt) * N + ee];
+        z += a.bias ? (double)a.bias[ee] : 0.0;
+        L.z[tt][ee] = z;
+        L.key[tt][ee] = logit_key(z);
+        if (a.logits_out && t0 + tt < a.T) a.logits_out[(size_t)(t0 + tt) * N + ee] = z;
+    }
+    __syncthreads();
+
+    // top-K: wave w ranks tokens w and w + 8 (rank of e = experts with a larger logit, or an
+    // equal one and a smaller id); then its wave takes the gates and classes
+    constexpr int kJ = SPICE_MAX_EXPERTS / 64;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int tt = w + h * kNW;
+        const unsigned long long* kr = L.key[tt];
+#pragma unroll
+        for (int j = 0; j < kJ; ++j) {
+            const int e = lane + 64 * j;
+            if (64 * j < N) {  // uniform
+                const unsigned long long ke = e < N ? kr[e] : 0ull;
+                int r = 0;
+#pragma unroll 8
+                for (int ee = 0; ee < N; ++ee) {
+                    const unsigned long long k2 = kr[ee];
+                    r += (int)((k2 > ke) | ((k2 == ke) & (ee < e)));
+                }
+                if (e < N && r < K) L.pick[tt][r] = e;
             }
         }
     }
+    __syncthreads();
+    // then the block's histogram of bucket keys
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int tt = w + h * kNW, t = t0 + tt;
+        if (t < a.T) {
+            const float conf_in = (a.conf_mode == SPICE_CONF_INPUT && lane < K) ? a.conf[(size_t)t * K + lane] : 0.f;
+            const int key = wave_topk_gates(a, t, L.z[tt], L.res, L.pick[tt], lane, conf_in);
+            if (key >= 0) atomicAdd(&L.hist[key], 1);
+        }
+    }
+    __syncthreads();
+    // as column blockIdx.x of the table
+    int* table = reinterpret_cast<int*>(a.logits_ws);
+    const int stride = prefill_hist_stride(a.T);
+    for (int k = tid; k < NK; k += kPrefillThreads) table[(size_t)k * stride + blockIdx.x] = L.hist[k];
 }
 
-// Top-K of the logits in the workspace: one block per token.
-__global__ __launch_bounds__(kLogitThreads) void route_topk_kernel(RouteArgs a) {
-    __shared__ TopkLds lds;
-    block_topk<kLogitThreads, false>(a, blockIdx.x, a.logits_ws + (size_t)blockIdx.x * a.N, lds);
+// One block: for each key, the exclusive running count over the routing blocks (in place)
+// and its total; the keys' starts (an exclusive scan over keys in order) to offsets, the
+// table's start row and the work lists; the class counts; then the host copies when asked.
+__global__ __launch_bounds__(kScanThreads) void bucket_scan_kernel(RouteArgs a) {
+    __shared__ int s_tot[3 * SPICE_MAX_EXPERTS];
+    __shared__ int s_start[3 * SPICE_MAX_EXPERTS];
+    __shared__ int s_wsum[kScanThreads / 64];
+    __shared__ int s_cls[3];
+    __shared__ int s_res[SPICE_MAX_EXPERTS];
+    constexpr int kNW = kScanThreads / 64;
+    constexpr int kGroup = 8;  // rows whose loads one round trip carries
+    const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+    const int N = a.N, NK = 3 * N;
+    const int nblk = (a.T + kPrefillTok - 1) / kPrefillTok, stride = prefill_hist_stride(a.T);
+    int* table = reinterpret_cast<int*>(a.logits_ws);
+    if (tid < 3) s_cls[tid] = 0;
+    const int res = (a.worklist && tid < N) ? a.resident_slot[tid] : -1;  // for the HIT work list
+    // wave w scans the rows of keys w, w + 16, ..., kGroup rows at a time: lane l holds
+    // columns 4l .. 4l+3 of a 256-column span, and a wave-wide inclusive scan gives each
+    // column's exclusive running count
+    for (int g0 = 0; g0 * kNW < NK; g0 += kGroup) {
+        int run[kGroup];
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) run[j] = 0;
+        for (int c0 = 0; c0 < stride; c0 += 256) {
+            const int col = c0 + 4 * lane;
+            int4 v[kGroup];
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) {
+                const int key = w + kNW * (g0 + j);
+                v[j] = (key < NK && col < stride) ? *reinterpret_cast<const int4*>(table + (size_t)key * stride + col)
+                                                  : make_int4(0, 0, 0, 0);
+            }
+#pragma unroll
+            for (int j = 0; j < kGroup; ++j) {
+                const int key = w + kNW * (g0 + j);
+                // columns past the last routing block hold garbage
+                const int x0 = col < nblk ? v[j].x : 0, x1 = col + 1 < nblk ? v[j].y : 0;
+                const int x2 = col + 2 < nblk ? v[j].z : 0, x3 = col + 3 < nblk ? v[j].w : 0;
+                const int mine = x0 + x1 + x2 + x3;
+                int incl = mine;
+#pragma unroll
+                for (int o = 1; o < 64; o <<= 1) {
+                    const int up = __shfl_up(incl, o);
+                    if (lane >= o) incl += up;
+                }
+                const int ex = run[j] + incl - mine;
+                if (key < NK && col < stride)
+                    *reinterpret_cast<int4*>(table + (size_t)key * stride + col) =
+                        make_int4(ex, ex + x0, ex + x0 + x1, ex + x0 + x1 + x2);
+                run[j] += __shfl(incl, 63);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < kGroup; ++j) {
+            const int key = w + kNW * (g0 + j);
+            if (key < NK && lane == 0) s_tot[key] = run[j];
+        }
+    }
+    __syncthreads();
+    const int tot = tid < NK ? s_tot[tid] : 0;
+    // exclusive scan of the totals over keys
+    int incl = tot;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int up = __shfl_up(incl, o);
+        if (lane >= o) incl += up;
+    }
+    if (lane == 63) s_wsum[w] = incl;
+    __syncthreads();
+    int start = incl - tot;
+    for (int ww = 0; ww < w; ++ww) start += s_wsum[ww];
+    if (tid < NK) {
+        s_start[tid] = start;
+        table[(size_t)NK * stride + tid] = start;
+        const int c = tid / N, e = tid - c * N;
+        a.offsets[c * (N + 1) + e] = start;
+        if (e == N - 1) a.offsets[c * (N + 1) + N] = start + tot;
+        if (tot) atomicAdd(&s_cls[c], tot);
+    }
+    if (tid < N) s_res[tid] = res;
+    __syncthreads();
+    if (tid < 3 && a.h_counts) a.h_counts[tid] = s_cls[tid];
+    // work lists: wave c (< 3) ranks the non-empty buckets of class c by expert id
+    if (a.worklist && w < 3) {
+        const int c = w;
+        int seen = 0;
+        const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+        for (int e0 = 0; e0 < N; e0 += 64) {
+            const int e = e0 + lane;
+            const int n = e < N ? s_tot[c * N + e] : 0;
+            const unsigned long long mk = __ballot(n > 0);
+            if (n > 0) {
+                int slot = -1;
+                if (c == SPICE_CLASS_HIT) {
+                    slot = s_res[e];
+                    if (slot < 0 || slot >= a.C) slot = -1;  // routing flagged it already
+                }
+                *reinterpret_cast<int4*>(a.worklist + 4 * (c * N + seen + __popcll(mk & lt))) =
+                    make_int4(e, slot, s_start[c * N + e], n);
+            }
+            seen += __popcll(mk);
+        }
+        if (lane == 0) a.wl_count[c] = seen;
+    }
+    if (a.hx || a.h_idx || a.h_w || a.h_cls || a.h_ready) {
+        __syncthreads();
+        mirror_host<kScanThreads>(a);
+    }
+}
+
+// Stable positions of the slots of tokens [16 b, 16 b + 16), by one wave: slot s with key k
+// goes to start[k] + (slots of key k in earlier blocks) + (earlier slots of key k here).
+__global__ __launch_bounds__(64) void bucket_scatter_kernel(RouteArgs a) {
+    __shared__ int s_run[3 * SPICE_MAX_EXPERTS];
+    const int lane = threadIdx.x;
+    const int N = a.N, NK = 3 * N, S = a.T * a.K;
+    const int stride = prefill_hist_stride(a.T);
+    const int* table = reinterpret_cast<const int*>(a.logits_ws);
+    for (int k = lane; k < NK; k += 64) s_run[k] = 0;
+    __syncthreads();
+    const int s0 = blockIdx.x * kPrefillTok * a.K, s1 = min(a.T, (blockIdx.x + 1) * kPrefillTok) * a.K;
+    const unsigned long long lt = (lane == 0) ? 0ull : (~0ull >> (64 - lane));
+    for (int c0 = s0; c0 < s1; c0 += 64) {  // chunks in slot order: ranks stay stable
+        const int s = c0 + lane;
+        const int key = s < s1 ? route_slot_key(a, s) : -1;
+        const bool valid = key >= 0;
+        const int base = valid ? table[(size_t)NK * stride + key] + table[(size_t)key * stride + blockIdx.x] : 0;
+        unsigned long long match = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 10; ++b) {
+            const bool bit = (key >> b) & 1;
+            const unsigned long long bb = __ballot(valid && bit);
+            match &= bit ? bb : ~bb;
+        }
+        if (valid) {
+            const int pos = base + s_run[key] + __popcll(match & lt);
+            if (pos >= 0 && pos < S) {
+                a.perm[pos] = s;
+                a.inv_perm[s] = pos;
+            } else {
+                atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+            }
+        }
+        __syncthreads();  // every lane has read s_run before the chunk's counts are added
+        if (valid && (match >> lane) == 1ull) s_run[key] += __popcll(match);
+        __syncthreads();
+    }
 }
 
 }  // namespace
@@ -120,14 +386,14 @@ hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
         else
             hipLaunchKernelGGL(route_logits_kernel<SPICE_F32>, grid, dim3(kLogitThreads), 0, s, a, g);
     } else {
-        const unsigned nb = (unsigned)((a.T + 15) / 16);
+        const unsigned nb = (unsigned)((a.T + kPrefillTok - 1) / kPrefillTok);
         if (a.dtype == SPICE_BF16)
-            hipLaunchKernelGGL(route_logits_mfma_kernel<SPICE_BF16>, dim3(nb), dim3(kMfmaThreads), 0, s, a);
+            hipLaunchKernelGGL(route_prefill_kernel<SPICE_BF16>, dim3(nb), dim3(kPrefillThreads), 0, s, a);
         else
-            hipLaunchKernelGGL(route_logits_mfma_kernel<SPICE_F32>, dim3(nb), dim3(kMfmaThreads), 0, s, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(route_topk_kernel, dim3((unsigned)a.T), dim3(kLogitThreads), 0, s, a);
+            hipLaunchKernelGGL(route_prefill_kernel<SPICE_F32>, dim3(nb), dim3(kPrefillThreads), 0, s, a);
+        hipLaunchKernelGGL(bucket_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, a);
+        hipLaunchKernelGGL(bucket_scatter_kernel, dim3(nb), dim3(64), 0, s, a);
+        return hipGetLastError();
     }
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;

@@ -178,17 +178,20 @@ struct TopkLds {
     int pick[64];
 };
 
-// The gates, confidence and classes of token t's K picks, by wave 0 of block_topk.
-__device__ void block_topk_gates(const RouteArgs& a, int t, const TopkLds& L, int lane, float conf_in) {
+// The gates, confidence and classes of token t's K picks, by one wave: z = its N logits,
+// res = resident_slot, pick = its experts in rank order (all in LDS).  Lane k < K returns
+// its slot's bucket key (class * N + expert), the other lanes -1.
+__device__ int wave_topk_gates(const RouteArgs& a, int t, const double* z, const int* res, const int* pick,
+                               int lane, float conf_in) {
     constexpr int kJ = SPICE_MAX_EXPERTS / 64;
     const int N = a.N, K = a.K;
-    const double m = L.z[L.pick[0]];  // the largest logit
+    const double m = z[pick[0]];  // the largest logit
     double part = 0.0;
 #pragma unroll
     for (int j = 0; j < kJ; ++j)
-        if (lane + 64 * j < N) part += exp(L.z[lane + 64 * j] - m);
-    const int my_e = lane < K ? L.pick[lane] : 0;
-    const double my_ex = lane < K ? exp(L.z[my_e] - m) : 0.0;
+        if (lane + 64 * j < N) part += exp(z[lane + 64 * j] - m);
+    const int my_e = lane < K ? pick[lane] : 0;
+    const double my_ex = lane < K ? exp(z[my_e] - m) : 0.0;
     const double denom = route_wave_sum(part);
     double g = my_ex / denom;
     if (a.norm_topk) g = g / route_wave_sum(lane < K ? g : 0.0);
@@ -199,7 +202,7 @@ __device__ void block_topk_gates(const RouteArgs& a, int t, const TopkLds& L, in
         if (a.conf_mode == SPICE_CONF_INPUT) conf = conf_in;
         else if (a.conf_mode == SPICE_CONF_GATE) conf = (float)g;
         else conf = (float)(g / gsum);
-        int32_t slot = L.res[my_e];
+        int32_t slot = res[my_e];
         if (slot < -1 || slot >= a.C) {
             atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_SLOT);
             slot = -1;
@@ -211,7 +214,9 @@ __device__ void block_topk_gates(const RouteArgs& a, int t, const TopkLds& L, in
         a.topk_idx[s] = my_e;
         a.topk_w[s] = (float)g;
         a.slot_class[s] = cls;
+        return cls * N + my_e;
     }
+    return -1;
 }
 
 // Top-K of token t from its N logits zg (fp64, bias included; global memory) by one block
@@ -260,7 +265,7 @@ __device__ void block_topk(const RouteArgs& a, int t, const double* zg, TopkLds&
     for (int e = tid; e < N; e += NT)
         if (L.rank[e] < K) L.pick[L.rank[e]] = e;
     __syncthreads();
-    if (w == 0) block_topk_gates(a, t, L, lane, conf_in);
+    if (w == 0) wave_topk_gates(a, t, L.z, L.res, L.pick, lane, conf_in);
 }
 
 // The last of a token's routing blocks to finish, found with an arrival counter.  A block's
