@@ -63,24 +63,9 @@ hipError_t launch_expert_ffn(const FfnArgs& f, hipStream_t s) {
     const bool hit = (a.groups & kDoHit) != 0;
     const bool shared = (a.groups & kDoShared) != 0 && a.Is > 0;
     const bool lore = (a.groups & kDoLore) != 0 && a.r > 0;
-    const int slots = a.T * a.K;
-    Grid up{0, 1, 0, 0, 1}, dn{0, 1, 0, 0, 1};
-    if (hit) {
-        up.nhit = dn.nhit = std::min(std::min(a.N, a.C), slots);
-        up.thit = (a.I + 15) / 16;
-        dn.thit = (a.d + 16 * kDownRows - 1) / (16 * kDownRows);
-    }
-    if (shared) {
-        up.tsh = (a.Is + 15) / 16;
-        dn.tsh = (a.d + 16 * kDownRows - 1) / (16 * kDownRows);
-    }
-    if (lore) {
-        up.nlore = dn.nlore = std::min(a.N, slots);
-        up.tlore = (a.r + 15) / 16;
-        dn.tlore = (a.d + kLoreRows - 1) / kLoreRows;
-    }
-    const long long nup = (long long)up.nhit * up.thit + up.tsh + (long long)up.nlore * up.tlore;
-    const long long ndn = (long long)dn.nhit * dn.thit + dn.tsh + (long long)dn.nlore * dn.tlore;
+    Grid up, dn;
+    ffn_grids(a, hit, shared, lore, up, dn);
+    const long long nup = up.blocks(), ndn = dn.blocks();
     if (nup == 0) return hipSuccess;
     if (a.dtype == SPICE_BF16) {
         hipLaunchKernelGGL(ffn_up_kernel<SPICE_BF16>, dim3((unsigned)nup), dim3(kThreads), 0, s, a, up);

@@ -401,24 +401,13 @@ hipError_t launch_expert_ffn_mx(const FfnArgs& a, hipStream_t s) {
     const bool hit = (a.groups & kDoHit) != 0;
     const bool shared = (a.groups & kDoShared) != 0 && a.Is > 0;
     const bool lore = (a.groups & kDoLore) != 0 && a.r > 0;
-    const int slots = a.T * a.K;
-    Grid up{0, 1, 0, 0, 1}, dn{0, 1, 0, 0, 1};
-    if (hit) {
-        up.nhit = dn.nhit = std::min(std::min(a.N, a.C), slots);
+    Grid up, dn;
+    ffn_grids(a, hit, shared, lore, up, dn);
+    if (hit) {  // the MXFP4 HIT tiles are taller
         up.thit = (a.I + 16 * kMxUpR - 1) / (16 * kMxUpR);
         dn.thit = (a.d + 16 * kMxDownR - 1) / (16 * kMxDownR);
     }
-    if (shared) {
-        up.tsh = (a.Is + 15) / 16;
-        dn.tsh = (a.d + 16 * kDownRows - 1) / (16 * kDownRows);
-    }
-    if (lore) {
-        up.nlore = dn.nlore = std::min(a.N, slots);
-        up.tlore = (a.r + 15) / 16;
-        dn.tlore = (a.d + kLoreRows - 1) / kLoreRows;
-    }
-    const long long nup = (long long)up.nhit * up.thit + up.tsh + (long long)up.nlore * up.tlore;
-    const long long ndn = (long long)dn.nhit * dn.thit + dn.tsh + (long long)dn.nlore * dn.tlore;
+    const long long nup = up.blocks(), ndn = dn.blocks();
     if (nup == 0) return hipSuccess;
     hipLaunchKernelGGL(ffn_up_mx_kernel, dim3((unsigned)nup), dim3(kThreads), 0, s, a, up);
     hipLaunchKernelGGL(ffn_down_mx_kernel, dim3((unsigned)ndn), dim3(kThreads), 0, s, a, dn);

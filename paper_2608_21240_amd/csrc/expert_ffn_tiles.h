@@ -9,16 +9,13 @@
 #include <algorithm>
 
 #include "spice_internal.h"
+#include "tile_index.h"
 
 namespace spice {
 namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = 4;
-constexpr int kTokTiles = 2;        // token tiles of 16 per pass
-constexpr int kDownRows = 2;        // 16-row tiles per down tile of a routed expert
-constexpr int kLoreRows = 256;      // B_e rows per LoRE tile (one per thread)
-constexpr int kLoreTok = 16;        // tokens per LoRE pass
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -77,10 +74,6 @@ __device__ __forceinline__ void Tr<SPICE_BF16>::store4(void* base, size_t elem, 
 
 __device__ __forceinline__ float silu(float u) { return u / (1.0f + __expf(-u)); }
 
-struct Group {
-    int e, start, n, slot;
-};
-
 // The j-th expert (ascending id) whose bucket of class c is non-empty; for HIT
 // buckets its pool slot is fetched in the same round trip as the offsets.
 __device__ __attribute__((unused)) bool find_group(const FfnArgs& a, int c, int j, Group& g) {
@@ -90,27 +83,21 @@ __device__ __attribute__((unused)) bool find_group(const FfnArgs& a, int c, int 
     int seen = 0;
     for (int base = 0; base < a.N; base += 64) {
         const int e = base + lane;
-        int st = 0, n = 0, slot = -1;
-        if (e < a.N) {
-            st = off[e];
-            n = off[e + 1] - st;
-            if (c == SPICE_CLASS_HIT) slot = a.resident_slot[e];
-        }
-        const unsigned long long m = __ballot(n > 0);
+        Group mine_g{e, 0, 0, -1};
+        if (e < a.N) mine_g = bucket_of(off, e, c, c == SPICE_CLASS_HIT ? a.resident_slot[e] : -1);
+        const unsigned long long m = __ballot(mine_g.n > 0);
         const int cnt = __popcll(m);
         if (j < seen + cnt) {
-            const bool mine = n > 0 && __popcll(m & lt) == j - seen;
+            const bool mine = mine_g.n > 0 && __popcll(m & lt) == j - seen;
             const int src = __ffsll((long long)__ballot(mine)) - 1;
             g.e = base + src;
-            g.start = __shfl(st, src);
-            g.n = __shfl(n, src);
-            g.slot = __shfl(slot, src);
-            if (g.start < 0 || g.n < 0 || g.start + g.n > a.T * a.K) {
-                if (lane == 0) atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
-                return false;
-            }
-            if (c == SPICE_CLASS_HIT && (g.slot < 0 || g.slot >= a.C)) {
-                if (lane == 0) atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_SLOT);
+            g.start = __shfl(mine_g.start, src);
+            g.n = __shfl(mine_g.n, src);
+            g.slot = __shfl(mine_g.slot, src);
+            if (!group_in_range(a, c, g)) {
+                const bool slot_bad = c == SPICE_CLASS_HIT && g.start >= 0 && g.n >= 0 && g.start + g.n <= a.T * a.K;
+                if (lane == 0)
+                    atomicOr(&a.ctrl[kWordFlags], (uint32_t)(slot_bad ? SPICE_FLAG_BAD_SLOT : SPICE_FLAG_BAD_INDEX));
                 return false;
             }
             return true;
@@ -119,29 +106,6 @@ __device__ __attribute__((unused)) bool find_group(const FfnArgs& a, int c, int 
     }
     return false;
 }
-
-enum : int { kKindHit = 0, kKindShared = 1, kKindLore = 2 };
-
-struct Tile {
-    int kind, ordinal, rt;
-};
-
-// Block index -> tile.  Segments, in dispatch order: shared-block row tiles (the
-// longest tiles: all T tokens, and the longest contraction in the down pass), LORE
-// experts x row tiles (short but latency-bound), HIT experts x row tiles.  Putting
-// the long tiles first keeps them out of the launch's tail.  Expert counts are upper
-// bounds; surplus blocks exit at once.
-struct Grid {
-    int nhit, thit, tsh, nlore, tlore;
-    __device__ bool decode(int b, Tile& t) const {
-        if (b < tsh) { t = {kKindShared, 0, b}; return true; }
-        b -= tsh;
-        if (b < nlore * tlore) { t = {kKindLore, b / tlore, b % tlore}; return true; }
-        b -= nlore * tlore;
-        if (b < nhit * thit) { t = {kKindHit, b / thit, b % thit}; return true; }
-        return false;
-    }
-};
 
 // ---------------------------------------------------------------------------
 // MFMA main loop shared by both launches.
@@ -153,7 +117,6 @@ struct Grid {
 // branches: its loads are unconditional and in order, and the wait before each MFMA
 // leaves the next group's loads in flight (two groups per wave).
 // ---------------------------------------------------------------------------
-constexpr int kStepBytes = 64;  // 32 bf16 or 16 fp32 per step per 4 lanes; same byte stride
 
 // Steps per load group: 4 with three operand streams (two weight tiles and one token tile,
 // or one and two), 2 with four; two groups are in flight, which fits 3 waves per SIMD.
@@ -375,44 +338,22 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, int rt, const int32_t*
     constexpr bool kUp = KIND != kKindLore;
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
-    const void* wbase;
-    size_t gate_row0, up_row0;
-    int nrows, start, n;
-    if constexpr (KIND == kKindHit) {
-        start = g.start;
-        n = g.n;
-        wbase = a.w13_pool;
-        nrows = a.I;
-        gate_row0 = (size_t)g.slot * 2 * a.I;
-        up_row0 = gate_row0 + a.I;
-    } else if constexpr (KIND == kKindShared) {
-        start = 0;
-        n = a.T;
-        wbase = a.w13s;
-        nrows = a.Is;
-        gate_row0 = 0;
-        up_row0 = a.Is;
-        ids = nullptr;
-    } else {
-        start = g.start;
-        n = g.n;
-        wbase = a.lore_A;
-        nrows = a.r;
-        gate_row0 = (size_t)g.e * a.r;
-        up_row0 = gate_row0;
-    }
+    const void* wbase = up_weights<KIND>(a);
+    const UpBlock ub = up_block<KIND>(a, g);
+    const int nrows = ub.nrows;
+    int start, n;
+    tile_entries<KIND>(a, g, start, n);
+    if constexpr (KIND == kKindShared) ids = nullptr;
     const int m = lane & 15;  // A row / B column owned by this lane
     const int quad = lane >> 4;
-    // rows past the end of the matrix read its last row; their outputs are dropped
-    const int row = min(rt * 16 + m, nrows - 1);
+    const int row = tile_row(rt, kTileRows, m, nrows);
     const size_t kb = (size_t)quad * T_::kLaneK * es;  // lane's byte offset inside a step
-    const char* gate = static_cast<const char*>(wbase) + (gate_row0 + row) * (size_t)a.d * es + kb;
-    const char* up = static_cast<const char*>(wbase) + (up_row0 + row) * (size_t)a.d * es + kb;
+    const char* gate = static_cast<const char*>(wbase) + (ub.gate_row0 + row) * (size_t)a.d * es + kb;
+    const char* up = static_cast<const char*>(wbase) + (ub.up_row0 + row) * (size_t)a.d * es + kb;
 
     for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
-        // padding columns read the bucket's last token; their outputs are dropped
-        const int gi0 = min(g0 + m, n - 1), gi1 = min(g0 + 16 + m, n - 1);
+        const int gi0 = tile_entry(g0, 0, m, n), gi1 = tile_entry(g0, 1, m, n);
         if (ntt == 1) up_pass<DT, 1, kUp>(a, gate, up, ids, gi0, gi1, kb, w, quad, red, lane);
         else up_pass<DT, 2, kUp>(a, gate, up, ids, gi0, gi1, kb, w, quad, red, lane);
         __syncthreads();
@@ -424,7 +365,7 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, int rt, const int32_t*
             const int gi = g0 + tt * 16 + m;  // output column = token of lane m
             const int orow = rt * 16 + quad * 4;
             if constexpr (KIND == kKindLore) {
-                if (gi < n && orow < nrows) *reinterpret_cast<f32x4_t*>(a.u + (size_t)(start + gi) * a.r + orow) = sg;
+                if (gi < n && orow < nrows) *reinterpret_cast<f32x4_t*>(a.u + up_out_elem<KIND>(a, start, gi, orow)) = sg;
             } else {
                 f32x4_t su = red[0][tt][1][lane];
 #pragma unroll
@@ -435,10 +376,7 @@ __device__ void up_tile(const FfnArgs& a, const Group& g, int rt, const int32_t*
                     h.y = silu(sg.y) * su.y;
                     h.z = silu(sg.z) * su.z;
                     h.w = silu(sg.w) * su.w;
-                    if constexpr (KIND == kKindHit)
-                        T_::store4(a.h, (size_t)(start + gi) * a.ldh + orow, h);
-                    else
-                        T_::store4(a.hs, (size_t)gi * a.ldhs + orow, h);
+                    T_::store4(KIND == kKindHit ? a.h : a.hs, up_out_elem<KIND>(a, start, gi, orow), h);
                 }
             }
         }
@@ -470,7 +408,7 @@ __device__ void lore_down_tile(const FfnArgs& a, int expert, int start, int n, i
     const int tid = threadIdx.x;
     const int row = rt * kLoreRows + tid;
     const bool row_ok = row < a.d;
-    const size_t brow = ((size_t)expert * a.d + (row_ok ? row : 0)) * (size_t)a.r;
+    const size_t brow = lore_b_elem(a, expert, row_ok ? row : 0, 0);
     const u32x4_t zero = {0u, 0u, 0u, 0u};
     for (int g0 = 0; g0 < n; g0 += kLoreTok) {
         const int nt = min(kLoreTok, n - g0);
@@ -486,7 +424,7 @@ __device__ void lore_down_tile(const FfnArgs& a, int expert, int start, int n, i
 #pragma unroll
             for (int i = 0; i < kUPer; ++i) {
                 const int idx = tid + i * kThreads, j = idx / kLoreChunk, q = idx - j * kLoreChunk;
-                uv[i] = (j < nt && q < nq) ? a.u[(size_t)(start + g0 + j) * a.r + q0 + q] : 0.f;
+                uv[i] = (j < nt && q < nq) ? a.u[lore_u_elem(a, start, g0 + j, q0 + q)] : 0.f;
             }
 #pragma unroll
             for (int i = 0; i < kUPer; ++i) s_u[tid + i * kThreads] = uv[i];
@@ -522,7 +460,7 @@ __device__ void lore_down_tile(const FfnArgs& a, int expert, int start, int n, i
         if (row_ok) {
 #pragma unroll
             for (int j = 0; j < kLoreTok; ++j)
-                if (j < nt) a.y_slots[(size_t)(start + g0 + j) * a.d + row] = acc[j];
+                if (j < nt) a.y_slots[lore_y_elem(a, start, g0 + j, row)] = acc[j];
         }
     }
 }
@@ -551,40 +489,25 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, int rt, f32x4_t (&re
     constexpr int es = (DT == SPICE_BF16) ? 2 : 4;
     const int lane = threadIdx.x & 63;
     const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // wave index, uniform
-    const void* wbase;
-    const void* hbase;
-    int kdim, start, n;
-    size_t row0, ld;
-    if constexpr (KIND == kKindHit) {
-        start = g.start;
-        n = g.n;
-        wbase = a.w2_pool;
-        hbase = a.h;
-        kdim = a.I;
-        row0 = (size_t)g.slot * a.d;
-        ld = a.ldh;
-    } else {
-        start = 0;
-        n = a.T;
-        wbase = a.w2s;
-        hbase = a.hs;
-        kdim = a.Is;
-        row0 = 0;
-        ld = a.ldhs;
-    }
+    const void* wbase = down_weights<KIND>(a);
+    const void* hbase = down_inputs<KIND>(a);
+    const DownBlock db = down_block<KIND>(a, g);
+    const int kdim = db.kdim;
+    int start, n;
+    tile_entries<KIND>(a, g, start, n);
     const int m = lane & 15, quad = lane >> 4;
-    const int dim0 = rt * 16 * R;
+    const int dim0 = rt * kTileRows * R;
     const size_t kb = (size_t)quad * T_::kLaneK * es;
     const char* const aw[kDownRows] = {
         // tail rows read the last row; their outputs are dropped
-        static_cast<const char*>(wbase) + (row0 + min(dim0 + m, a.d - 1)) * (size_t)kdim * es + kb,
-        static_cast<const char*>(wbase) + (row0 + min(dim0 + 16 + m, a.d - 1)) * (size_t)kdim * es + kb};
+        static_cast<const char*>(wbase) + (db.row0 + tile_row(rt, kTileRows * R, m, a.d)) * (size_t)kdim * es + kb,
+        static_cast<const char*>(wbase) + (db.row0 + tile_row(rt, kTileRows * R, kTileRows + m, a.d)) * (size_t)kdim * es + kb};
     const char* const a1[1] = {aw[0]};
     for (int g0 = 0; g0 < n; g0 += 16 * kTokTiles) {
         const int ntt = min(kTokTiles, (n - g0 + 15) / 16);
         const char* const hb[kTokTiles] = {
-            static_cast<const char*>(hbase) + (size_t)(start + min(g0 + m, n - 1)) * ld * es + kb,
-            static_cast<const char*>(hbase) + (size_t)(start + min(g0 + 16 + m, n - 1)) * ld * es + kb};
+            static_cast<const char*>(hbase) + (size_t)(start + tile_entry(g0, 0, m, n)) * db.ld * es + kb,
+            static_cast<const char*>(hbase) + (size_t)(start + tile_entry(g0, 1, m, n)) * db.ld * es + kb};
         const char* const h1[1] = {hb[0]};
         if constexpr (R == 1) {
             if (ntt == 1) down_pass<DT, 1, 1>(a1, h1, kdim, w, quad, red, lane);
@@ -605,9 +528,9 @@ __device__ void down_tile(const FfnArgs& a, const Group& g, int rt, f32x4_t (&re
             if (gi < n && dim < a.d) {
                 if constexpr (KIND == kKindShared) {
                     if (a.sgate) s *= a.sgate[gi];  // gated shared block
-                    *reinterpret_cast<f32x4_t*>(a.y_shared + (size_t)gi * a.d + dim) = s;
+                    *reinterpret_cast<f32x4_t*>(a.y_shared + down_out_elem<KIND>(a, start, gi, dim)) = s;
                 } else {
-                    *reinterpret_cast<f32x4_t*>(a.y_slots + (size_t)(start + gi) * a.d + dim) = s;
+                    *reinterpret_cast<f32x4_t*>(a.y_slots + down_out_elem<KIND>(a, start, gi, dim)) = s;
                 }
             }
         }
