@@ -41,21 +41,35 @@ sys.path.insert(0, ROOT)
 HBM_PEAK_GBS = 8000.0
 METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shaped"
 
-# HBM traffic of one grouped-FFN call (up + down kernels) at the headline batch, from
+# HBM traffic per call of the layer's GPU path and of the grouped-FFN call at the headline batch, from
 # two rocprofv3 --pmc passes over this script (FETCH_SIZE, then WRITE_SIZE; KiB per
 # dispatch) scaled by what the counters read for a plain 1 GiB device copy
 # (FETCH_SIZE x2.0, WRITE_SIZE x1.0).  One record per expert weight format; each is
 # reported only while the kernel sources (the files hashed together) are the ones the
 # counters were taken on.
 TRAFFIC_RECORDS = {
-    "bf16": {
-        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
-        "source_sha256_16": "a34166ed9f8959c3",
-        "fetch_kib_per_call": 189122.92 + 96783.86,
-        "write_kib_per_call": 462.50 + 1451.88,
+    # the layer's GPU path at T = 32: layer_route + layer_up + layer_down + combine
+    "layer_bf16": {
+        "kernel_sources": ("paper_2608_21240_amd/csrc/layer_decode.hip", "paper_2608_21240_amd/csrc/route_device.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h", "paper_2608_21240_amd/csrc/tile_index.h",
+                           "paper_2608_21240_amd/csrc/combine.hip"),
+        "source_sha256_16": "a78dec8c8d42b2e5",
+        "fetch_kib_per_call": 12042.6 + 184115.6 + 90271.8 + 905.8,
+        "write_kib_per_call": 260.1 + 675.8 + 1195.7 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
-        "profile": "profiles/ffn_dsv2_decode_T32_counters.md",
+        "profile": "profiles/layer_dsv2_decode_kernel_trace_counters.md",
+    },
+    # the grouped-FFN call alone at T = 32: ffn_up + ffn_down
+    "bf16": {
+        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
+                           "paper_2608_21240_amd/csrc/tile_index.h"),
+        "source_sha256_16": "43e1a297d6387968",
+        "fetch_kib_per_call": 189105.5 + 96795.6,
+        "write_kib_per_call": 462.4 + 1452.0,
+        "fetch_factor": 2.0,
+        "write_factor": 1.0,
+        "profile": "profiles/layer_dsv2_decode_kernel_trace_counters.md",
     },
     "mxfp4": {
         "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn_mx.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
@@ -647,7 +661,8 @@ def prefill_main(args):
     t_gen = time.time()
     host = LY.HostLayer(wl, 0)
     dev = LY.DeviceLayer(host, host_exact=args.resident < s.n_experts)
-    run = LY.LayerRun(s, T, dev.C, tau=wl.tau)
+    # separate routing and FFN calls, so that events can bracket the FFN launch
+    run = LY.LayerRun(s, T, dev.C, tau=wl.tau, layer_call=False)
     x = LY.to_tensor(synth.gen_x(wl, 0, 0, T), s.dtype, "cuda")
     conf = torch.from_numpy(synth.gen_conf(wl, 0, 0, T)).cuda()
     exact = args.resident < s.n_experts
@@ -663,7 +678,7 @@ def prefill_main(args):
     for _ in range(args.warmup):
         run.forward(dev, x, conf, T, exact=exact, n_threads=args.threads)
     torch.cuda.synchronize()
-    names = ("start", "routed", "ffn0", "experts", "resid", "end")
+    names = ("start", "routed", "experts", "resid", "end")
     evs = [{n: torch.cuda.Event(enable_timing=True) for n in names} for _ in range(args.steps)]
     t0 = time.perf_counter()
     for k in range(args.steps):
@@ -672,7 +687,8 @@ def prefill_main(args):
     wall = time.perf_counter() - t0
     if run.flags() != 0:
         raise RuntimeError("device flags raised")
-    ffn_ms = np.array([e["ffn0"].elapsed_time(e["experts"]) for e in evs])
+    ffn_ms = np.array([e["routed"].elapsed_time(e["experts"]) for e in evs])
+    route_us = float(np.median([e["start"].elapsed_time(e["routed"]) for e in evs]) * 1e3)
     achieved = flops / (ffn_ms.mean() * 1e-3) / 1e12
     line = {
         "metric": "MoE-layer prefill tokens/s + grouped-FFN MFMA TFLOP/s (% peak), Qwen2-57B-A14B-shaped",
@@ -688,6 +704,7 @@ def prefill_main(args):
                      "achieved": round(achieved, 1), "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(achieved / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
                      "flop_per_launch": flops, "avg_launch_us": round(float(ffn_ms.mean() * 1e3), 1)},
+        "route_us": round(route_us, 1),
         "classes": np.bincount(cls.ravel(), minlength=3).tolist(),
     }
     print(json.dumps(line), flush=True)
