@@ -854,7 +854,18 @@ def qwen2_records(args):
     torch.cuda.synchronize()
     layer_ms = float(np.median([a.elapsed_time(d) for a, b, c, d in evs]))
     ffn_ms = float(np.median([b.elapsed_time(c) for a, b, c, d in evs]))
-    route_ms = float(np.median([a.elapsed_time(b) for a, b, c, d in evs]))
+    # the routing alone: average over back-to-back calls from one event pair (behind a spin
+    # kernel, so that no span holds host submission time)
+    reps = 30
+    ra, rb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    torch.cuda._sleep(int(2e7))
+    ra.record()
+    for _ in range(reps):
+        run.route(dev, x, conf, T, to_host=False)
+    rb.record()
+    torch.cuda.synchronize()
+    route_ms = ra.elapsed_time(rb) / reps
     out["prefill_T4096"] = {
         "tokens": T, "resident": 64, "layer_ms": round(layer_ms, 3), "tokens_per_s": round(T / (layer_ms * 1e-3), 1),
         "route_us": round(route_ms * 1e3, 1), "ffn_ms": round(ffn_ms, 3), "flop_per_ffn_call": flops,

@@ -76,38 +76,41 @@ struct PrefillLds {
 // q*V .. q*V + V-1 of a 4V-wide k chunk, and MFMA step u takes element u of every lane, so
 // the 4 k of step u are {u, V + u, 2V + u, 3V + u} for both operands and each chunk's
 // products are all summed once.  A pass is two chunks; the next pass's loads are in flight
-// while one multiplies.  Rows beyond N and tokens beyond T load zero; d is a multiple of V.
+// while one multiplies.  d is a multiple of V.
 template <int DT>
-__device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr, bool tok_ok, int tile0, int ntg,
+__device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr, int tile0, int ntg,
                                               int p0, int p1, int lane, f64x4_t (&out)[4]) {
     using E = RouteElem<DT>;
     constexpr int V = E::V, es = E::es;
     const int m = lane & 15, q = lane >> 4;
     const char* wr[4];
-    bool e_ok[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int e = (tile0 + i) * 16 + m;
-        e_ok[i] = i < ntg && e < a.N;
-        wr[i] = static_cast<const char*>(a.wg) + (size_t)(e_ok[i] ? e : 0) * a.d * es;
+        wr[i] = static_cast<const char*>(a.wg) + (size_t)(i < ntg && e < a.N ? e : 0) * a.d * es;
     }
     f64x4_t acc[4][2] = {};
+    // Loads are unconditional, from clamped addresses: rows past N and tokens past T read
+    // row 0 / token 0 (finite values whose products land only in dropped outputs), and
+    // chunks past d read chunk 0 of the row, whose x is zeroed where it is used.  A select
+    // at the load would make every pass wait for the next pass's loads to land.
     auto load = [&](int p, uint4 (&xb)[2], uint4 (&wb)[4][2]) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int k = p * 8 * V + c * 4 * V + q * V;
-            const bool in = k < a.d;
-            const size_t kk = (size_t)(in ? k : 0) * es;  // out-of-range chunks load chunk 0 as zeros
-            xb[c] = load16_or_zero(xr + kk, in && tok_ok);
+            const size_t kk = (size_t)(k < a.d ? k : 0) * es;
+            xb[c] = *reinterpret_cast<const uint4*>(xr + kk);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) wb[i][c] = load16_or_zero(wr[i] + kk, in && e_ok[i]);
+            for (int i = 0; i < 4; ++i) wb[i][c] = *reinterpret_cast<const uint4*>(wr[i] + kk);
         }
     };
-    auto mul = [&](const uint4 (&xb)[2], const uint4 (&wb)[4][2]) {
+    auto mul = [&](int p, const uint4 (&xb)[2], const uint4 (&wb)[4][2]) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
+            const int k = p * 8 * V + c * 4 * V + q * V;
+            const uint4 zero = {0u, 0u, 0u, 0u};
             double xd[V];
-            E::widen(xb[c], xd);
+            E::widen(k < a.d ? xb[c] : zero, xd);
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 if (i < ntg) {  // uniform
@@ -126,11 +129,11 @@ __device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr
         int p = p0;
         for (; p + 1 < p1; p += 2) {
             load(p + 1, xb, wb);
-            mul(xa, wa);
+            mul(p, xa, wa);
             load(min(p + 2, p1 - 1), xa, wa);  // past the end: reloads the last pass, unused
-            mul(xb, wb);
+            mul(p + 1, xb, wb);
         }
-        if (p < p1) mul(xa, wa);
+        if (p < p1) mul(p, xa, wa);
     }
 #pragma unroll
     for (int i = 0; i < 4; ++i) out[i] = acc[i][0] + acc[i][1];
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArg
         const int g = w / parts, kp = w - g * parts;
         const int ntg = min(4, ntile - 4 * g);
         f64x4_t part[4];
-        prefill_group<DT>(a, xr, tok_ok, 4 * g, ntg, kp * npass / parts, (kp + 1) * npass / parts, lane, part);
+        prefill_group<DT>(a, xr, 4 * g, ntg, kp * npass / parts, (kp + 1) * npass / parts, lane, part);
         // result layout of the f64 16x16x4 product: element v of lane (m, q) is expert
         // tile*16 + 4v + q for token t0 + m
 #pragma unroll
