@@ -256,7 +256,8 @@ spice_status_t moe_combine(const spice_moe_cfg_t* cfg, int32_t T, const float* t
  * moe_expert_ffn_grouped_gated when w_shared_gate != NULL), then, if out != NULL, the
  * combine with `resid` (as moe_combine).  Every output is the one those calls define.
  * The work that does not depend on routing is not ordered after it (Sec. 4.2: the shared
- * block S is always resident): for dtype experts with T <= 256 and T*K <= 1024 the call is
+ * block S is always resident): for T <= 256 and T*K <= 1024 (routed experts in the cfg
+ * dtype or in MXFP4; bf16 dtype experts only while the prefill GEMMs do not apply) the call is
  * three launches in which routing runs beside the shared block's up projection, the
  * shared block's down projection beside the routed up projections, and each routed tile
  * finds its bucket from the routing itself; otherwise the separate launches of those calls.

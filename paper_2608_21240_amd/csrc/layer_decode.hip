@@ -17,6 +17,7 @@
 // Only a token's routing blocks wait for each other (through the counter, never by
 // spinning).  Up and down tiles are the grouped-FFN tile code (expert_ffn_tiles.h) with the
 // tile kind fixed at compile time.
+#include "expert_ffn_mx_tiles.h"
 #include "expert_ffn_tiles.h"
 #include "route_device.h"
 
@@ -31,11 +32,20 @@ constexpr int kLocalPer = 4;
 static_assert(kLayerMaxSlots == kLocalPer * kThreads, "local bucketing covers kLayerMaxSlots slots");
 
 // LDS of a launch-B block, in ints: the bucketing block's tables, or an up tile's reduction
-// buffer plus the local bucketing tables.
+// buffer (and, for MXFP4 HIT tiles, their scale stage) plus the local bucketing tables.
+constexpr int kMaxI(int a, int b) { return a > b ? a : b; }
 constexpr int kRedInts = kWaves * kTokTiles * 2 * 64 * 4;  // f32x4_t red[kWaves][kTokTiles][2][64]
+constexpr int kMxUpInts = (int)((sizeof(MxUpLds<kMxUpR>) + 15) / 16 * 4);
 constexpr int kLocalInts = 3 * SPICE_MAX_EXPERTS + SPICE_MAX_EXPERTS + 2 * kLayerMaxSlots + 4;
 constexpr int kBucketInts = (int)(bucket_lds_bytes(kThreads, SPICE_MAX_EXPERTS, kLayerMaxSlots) / sizeof(int));
-constexpr int kUpLdsInts = kRedInts + kLocalInts > kBucketInts ? kRedInts + kLocalInts : kBucketInts;
+template <bool kMx>
+constexpr int up_region_ints() { return kMx ? kMaxI(kRedInts, kMxUpInts) : kRedInts; }
+template <bool kMx>
+constexpr int up_lds_ints() { return kMaxI(up_region_ints<kMx>() + kLocalInts, kBucketInts); }
+// LDS of a launch-C block: a down tile's reduction buffer (and the MXFP4 scale stage).
+constexpr int kDownF4 = kWaves * kDownRows * kTokTiles * 64;
+template <bool kMx>
+constexpr int down_lds_f4() { return kMx ? kMaxI(kDownF4, (int)((sizeof(MxDownLds<kMxDownR>) + 15) / 16)) : kDownF4; }
 
 struct LayerGridA {
     int nroute, g_per_tok, tsh;
@@ -178,10 +188,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     up_tile<DT, kKindShared>(f, g, b - gr.nroute, nullptr, red);
 }
 
-template <int DT>
+template <int DT, bool kMx>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void layer_up_kernel(
     RouteArgs r, FfnArgs f, LayerGridB gr) {
-    __shared__ __align__(16) int lds[kUpLdsInts];
+    __shared__ __align__(16) int lds[up_lds_ints<kMx>()];
     int b = blockIdx.x;
     if (b == 0) {
         bucket_slots<kThreads, kLayerMaxSlots>(r, lds);
@@ -196,7 +206,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     }
     b -= gr.tsh_dn;
     auto& red = *reinterpret_cast<f32x4_t(*)[kWaves][kTokTiles][2][64]>(lds);
-    int* s_ids = lds + kRedInts;
+    int* s_ids = lds + up_region_ints<kMx>();
     int* s_loc = s_ids + kLayerMaxSlots;
     Group g;
     if (b < gr.nlore * gr.tlore) {
@@ -207,14 +217,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     b -= gr.nlore * gr.tlore;
     if (b < gr.nhit * gr.thit) {
         if (!local_group(f, r, SPICE_CLASS_HIT, b / gr.thit, g, s_loc, s_ids)) return;
-        up_tile<DT, kKindHit>(f, g, b % gr.thit, s_ids, red);
+        if constexpr (kMx) mx_up_tile<kMxUpR>(f, g, b % gr.thit, s_ids, *reinterpret_cast<MxUpLds<kMxUpR>*>(lds));
+        else up_tile<DT, kKindHit>(f, g, b % gr.thit, s_ids, red);
     }
 }
 
-template <int DT>
+template <int DT, bool kMx>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void layer_down_kernel(
     RouteArgs r, FfnArgs f, LayerGridC gr) {
-    __shared__ f32x4_t red[kWaves][kDownRows][kTokTiles][64];
+    __shared__ f32x4_t lds[down_lds_f4<kMx>()];
+    auto& red = *reinterpret_cast<f32x4_t(*)[kWaves][kDownRows][kTokTiles][64]>(lds);
     int b = blockIdx.x;
     Group g;
     if (b < gr.nlore * gr.tlore) {
@@ -225,7 +237,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     b -= gr.nlore * gr.tlore;
     if (b < gr.nhit * gr.thit) {
         if (!work_group(f, r, SPICE_CLASS_HIT, b / gr.thit, g)) return;
-        if (gr.rows16) down_tile<DT, kKindHit, 1>(f, g, b % gr.thit, red);
+        if constexpr (kMx) mx_down_tile<kMxDownR>(f, g, b % gr.thit, *reinterpret_cast<MxDownLds<kMxDownR>*>(lds));
+        else if (gr.rows16) down_tile<DT, kKindHit, 1>(f, g, b % gr.thit, red);
         else down_tile<DT, kKindHit>(f, g, b % gr.thit, red);
     }
 }
@@ -240,22 +253,31 @@ hipError_t launch_layer_decode(const RouteArgs& r, const FfnArgs& f, hipStream_t
     // the shared block's down tiles take 16 rows (twice as many, half as long: they would
     // otherwise be the longest tiles of the launch at small T); so do the HIT down tiles
     // while the batch is small (few experts, so too few tiles to fill the GPU)
+    const bool mx = f.wfmt == SPICE_WFMT_MXFP4;
+    if (mx && f.dtype != SPICE_BF16) return hipErrorInvalidValue;
     const bool rows16 = f.T <= kDownRows16MaxT;
+    // HIT tiles: MXFP4 tiles are 2 x 16 W1/W3 rows (up) and 4 x 16 W2 rows (down)
+    const int thit_up = mx ? (f.I + 16 * kMxUpR - 1) / (16 * kMxUpR) : (f.I + 15) / 16;
+    const int thit_dn = mx ? (f.d + 16 * kMxDownR - 1) / (16 * kMxDownR)
+                           : (rows16 ? (f.d + 15) / 16 : (f.d + 16 * kDownRows - 1) / (16 * kDownRows));
     LayerGridB gb{shared ? (f.d + 15) / 16 : 0, lore ? std::min(f.N, S) : 0, (f.r + 15) / 16,
-                  f.C > 0 ? std::min(std::min(f.N, f.C), S) : 0, (f.I + 15) / 16};
-    LayerGridC gc{gb.nlore, (f.d + kLoreRows - 1) / kLoreRows, gb.nhit,
-                  rows16 ? (f.d + 15) / 16 : (f.d + 16 * kDownRows - 1) / (16 * kDownRows), rows16 ? 1 : 0};
+                  f.C > 0 ? std::min(std::min(f.N, f.C), S) : 0, thit_up};
+    LayerGridC gc{gb.nlore, (f.d + kLoreRows - 1) / kLoreRows, gb.nhit, thit_dn, (!mx && rows16) ? 1 : 0};
     const unsigned na = (unsigned)(ga.nroute + ga.tsh);
     const unsigned nb = (unsigned)(1 + gb.tsh_dn + gb.nlore * gb.tlore + gb.nhit * gb.thit);
     const unsigned nc = (unsigned)(gc.nlore * gc.tlore + gc.nhit * gc.thit);
-    if (f.dtype == SPICE_BF16) {
+    if (mx) {
         hipLaunchKernelGGL(layer_route_kernel<SPICE_BF16>, dim3(na), dim3(kThreads), 0, s, r, f, ga);
-        hipLaunchKernelGGL(layer_up_kernel<SPICE_BF16>, dim3(nb), dim3(kThreads), 0, s, r, f, gb);
-        if (nc) hipLaunchKernelGGL(layer_down_kernel<SPICE_BF16>, dim3(nc), dim3(kThreads), 0, s, r, f, gc);
+        hipLaunchKernelGGL((layer_up_kernel<SPICE_BF16, true>), dim3(nb), dim3(kThreads), 0, s, r, f, gb);
+        if (nc) hipLaunchKernelGGL((layer_down_kernel<SPICE_BF16, true>), dim3(nc), dim3(kThreads), 0, s, r, f, gc);
+    } else if (f.dtype == SPICE_BF16) {
+        hipLaunchKernelGGL(layer_route_kernel<SPICE_BF16>, dim3(na), dim3(kThreads), 0, s, r, f, ga);
+        hipLaunchKernelGGL((layer_up_kernel<SPICE_BF16, false>), dim3(nb), dim3(kThreads), 0, s, r, f, gb);
+        if (nc) hipLaunchKernelGGL((layer_down_kernel<SPICE_BF16, false>), dim3(nc), dim3(kThreads), 0, s, r, f, gc);
     } else {
         hipLaunchKernelGGL(layer_route_kernel<SPICE_F32>, dim3(na), dim3(kThreads), 0, s, r, f, ga);
-        hipLaunchKernelGGL(layer_up_kernel<SPICE_F32>, dim3(nb), dim3(kThreads), 0, s, r, f, gb);
-        if (nc) hipLaunchKernelGGL(layer_down_kernel<SPICE_F32>, dim3(nc), dim3(kThreads), 0, s, r, f, gc);
+        hipLaunchKernelGGL((layer_up_kernel<SPICE_F32, false>), dim3(nb), dim3(kThreads), 0, s, r, f, gb);
+        if (nc) hipLaunchKernelGGL((layer_down_kernel<SPICE_F32, false>), dim3(nc), dim3(kThreads), 0, s, r, f, gc);
     }
     return hipGetLastError();
 }

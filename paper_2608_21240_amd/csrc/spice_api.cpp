@@ -570,8 +570,8 @@ spice_status_t moe_layer_gpu(const spice_moe_cfg_t* cfg, int32_t T, const void* 
         return st;
     const bool gated = w_shared_gate && c.shared_inter > 0;
     hipError_t e;
-    if (c.wfmt == SPICE_WFMT_DTYPE && T <= spice::kRouteTokenMaxT && T * c.top_k <= spice::kLayerMaxSlots &&
-        !spice::expert_gemm_applies(f)) {
+    if (T <= spice::kRouteTokenMaxT && T * c.top_k <= spice::kLayerMaxSlots &&
+        (c.wfmt == SPICE_WFMT_MXFP4 || !spice::expert_gemm_applies(f))) {
         if (gated) {
             float* sg = reinterpret_cast<float*>(static_cast<char*>(ws) + spice::ws_layout(c, T).sgate);
             r.w_sg = w_shared_gate;

@@ -178,7 +178,7 @@ hipError_t launch_expert_gemm(const FfnArgs& a, bool hit, bool shared, hipStream
 
 hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s);
 // The fused decode layer (routing, bucketing, shared block, HIT and LoRE FFN) in three
-// launches; bf16/fp32 experts, T <= kRouteTokenMaxT, T*K <= kLayerMaxSlots.
+// launches; bf16/fp32 or MXFP4 routed experts, T <= kRouteTokenMaxT, T*K <= kLayerMaxSlots.
 hipError_t launch_layer_decode(const RouteArgs& r, const FfnArgs& f, hipStream_t s);
 hipError_t launch_expert_ffn(const FfnArgs& a, hipStream_t s);
 // The same launch with MXFP4 routed experts (expert_ffn_mx.hip).

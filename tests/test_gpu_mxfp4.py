@@ -3,7 +3,8 @@ grouped FFN decodes the pool's blobs with the gfx950 scaled conversion, the host
 decodes the host blobs, and both are checked against the oracle's layer on the same
 blobs.  Shapes: reduced layers whose rows end in a partial group of MX blocks (K/32 not a
 multiple of 4), a 300-token call (many tokens per expert), and the DeepSeek-V2-Lite-shaped
-decode batches."""
+decode batches, each through the fused decode layer call and through the separate
+routing and FFN calls."""
 import numpy as np
 import pytest
 import torch
@@ -32,12 +33,15 @@ def mx(shape, T, R, **kw):
     return W.Workload("mxfp4", shape, tokens=T, resident=R, skew=kw.pop("skew", False), wfmt=W.WFMT_MXFP4, **kw)
 
 
+@pytest.mark.parametrize("layer_call", [True, False])
 @pytest.mark.parametrize("shape,T,R,fused", [(MX_A, 37, 6, True), (MX_A, 5, 9, False), (MX_B, 23, 5, True),
                                              (MX_B, 300, 8, True)])
-def test_mxfp4_layers(shape, T, R, fused):
-    say(f"mxfp4 d={shape.d} I={shape.inter} T={T} R={R} fused={fused}")
+def test_mxfp4_layers(shape, T, R, fused, layer_call):
+    """layer_call: the fused decode layer call (moe_layer_gpu; at T = 300 it takes the
+    separate launches), else the separate routing and FFN calls."""
+    say(f"mxfp4 d={shape.d} I={shape.inter} T={T} R={R} fused={fused} layer_call={layer_call}")
     c = Case(mx(shape, T, R))
-    c.run_gpu(fused=fused)
+    c.run_gpu(fused=fused, layer_call=layer_call)
     c.run_oracle()
     c.check_routing()
     c.check_outputs()
@@ -78,12 +82,13 @@ def dsv2_mx():
     return wl, host, dev
 
 
+@pytest.mark.parametrize("layer_call", [True, False])
 @pytest.mark.parametrize("T,tokens", [(1, None), (8, [0, 3, 7]), (32, [0, 9, 20, 31])])
-def test_dsv2_mxfp4_decode(dsv2_mx, T, tokens):
+def test_dsv2_mxfp4_decode(dsv2_mx, T, tokens, layer_call):
     wl, host, dev = dsv2_mx
-    say(f"dsv2 mxfp4 decode T={T}")
+    say(f"dsv2 mxfp4 decode T={T} layer_call={layer_call}")
     c = Case(wl.with_(tokens=T), host=host)
-    c.run_gpu(dev=dev)
+    c.run_gpu(dev=dev, layer_call=layer_call)
     c.run_oracle(tokens=tokens)
     c.check_routing()
     c.check_outputs()
