@@ -95,8 +95,11 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--calib-copy-mib", type=int, default=0,
                    help="finish with a plain device copy of this many MiB (a known-size reference for counters)")
-    p.add_argument("--workload", default="dsv2_decode", choices=("dsv2_decode", "qwen2_prefill", "dsv2_stack", "lore_fit"),
-                   help="dsv2_decode: the decode layer (default); qwen2_prefill: the 4096-token "
+    p.add_argument("--workload", default="dsv2_decode",
+                   choices=("dsv2_decode", "qwen2_decode", "qwen2_prefill", "dsv2_stack", "lore_fit"),
+                   help="dsv2_decode: the decode layer (default); qwen2_decode: the Qwen2-57B-A14B-shaped "
+                        "decode batch (T=16) at 16/32/48 resident experts and the prefill record only; "
+                        "qwen2_prefill: the 4096-token "
                         "Qwen2-57B-A14B-shaped layer on the MFMA GEMM path; dsv2_stack: the 26-layer "
                         "LRU-cached decode stack with and without speculative prefetching; lore_fit: "
                         "LoRE calibration fits of DSV2-Lite experts (512 tokens, rank 32)")
@@ -258,6 +261,20 @@ def main():
     torch.cuda.set_device(0)
     if args.workload == "qwen2_prefill":
         return prefill_main(args)
+    if args.workload == "qwen2_decode":
+        rec = qwen2_records(args)
+        r32 = rec["decode_T16"]["R32"]
+        print(json.dumps({
+            "metric": "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), Qwen2-57B-A14B-shaped",
+            "value": r32["tokens_per_s"], "unit": "tokens/s", "n_gpus": 1, "steps": None, "warmup": None,
+            "ms_per_step": round(r32["avg_call_us"] / 1e3, 4), "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded random-init Qwen2-57B-A14B-shaped layer)",
+            "config": {"workload": "qwen2_57b_a14b_moe_layer_decode_T16_R32", "resident": 32, "tokens": 16},
+            "roofline": {"bound": "hbm", "kernel": "the layer's GPU path, one moe_layer_gpu call with the combine",
+                         "achieved": r32["GBps"], "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": r32["frac"],
+                         "traffic": None},
+            "qwen2": rec}), flush=True)
+        return
     if args.workload == "dsv2_stack":
         return stack_main(args)
     if args.workload == "lore_fit":
