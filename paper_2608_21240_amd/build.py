@@ -62,6 +62,13 @@ def build(verbose: bool = False) -> str:
     if verbose:
         print(" ".join(link), flush=True)
     subprocess.run(link, check=True)
+    # A kernel whose host pass is rejected loses its launch stub without an error and the
+    # shared library still links; refuse such a library here rather than at load time.
+    undef = subprocess.run(["nm", "-D", "--undefined-only", tmp], check=True, capture_output=True, text=True).stdout
+    missing = [l.split()[-1] for l in undef.splitlines() if "__device_stub__" in l]
+    if missing:
+        os.remove(tmp)
+        raise RuntimeError("kernels without a host launch stub: " + ", ".join(missing))
     os.replace(tmp, LIB)
     return LIB
 

@@ -5,18 +5,21 @@
 //   up   : H[pos][f] = silu(sum_k W1[f][k] x[k]) * (sum_k W3[f][k] x[k])   (bf16 out)
 //   down : Y[pos][j] = sum_k W2[j][k] H[pos][k]                            (fp32 out)
 //
-// Block tile: 256 weight rows x 256 tokens, 64 k per stage, 4 waves of 128 x 128
-// (the accumulators live in AGPRs; LDS traffic is 64 flop per byte read).
-// For `up` the 256 weight rows are 128 W1 rows and the same 128 W3 rows, so each
-// wave holds the gate and up sums of its 64 features and applies SwiGLU in
-// registers.  The weight tile is the MFMA A operand and the token tile the B
-// operand (v_mfma_f32_16x16x32_bf16): a lane ends with 4 consecutive features of
-// one token, stored with one 8- (bf16) or 16-byte (fp32) write.
+// Block tile: 256 weight rows x 256 tokens, 64 k per stage, 8 waves of 128 weight rows x
+// 64 tokens (LDS traffic is 43 flop per byte read).  For `up` the 256 weight rows are 128
+// W1 rows and the same 128 W3 rows, so each wave holds the gate and up sums of its 64
+// features and applies SwiGLU in registers.  The weight tile is the MFMA A operand and
+// the token tile the B operand (v_mfma_f32_16x16x32_bf16): a lane ends with 4 consecutive
+// features of one token, stored with one 8- (bf16) or 16-byte (fp32) write.  A wave's
+// token sub-tiles are interleaved with the other waves' (rows 64 t + 16 wt), so the ragged
+// last tile of an expert spreads over the SIMDs and sub-tiles without a live token issue
+// no MFMA.
 // Both tiles are staged through LDS (two stages, 128 KiB: one block per CU) in
 // 128-byte rows whose 16-byte chunks are XOR-swizzled by row (chunk c of row r at
-// c ^ ((r >> 1) & 7)), so fragment reads and staging writes are free of bank
-// conflicts.  Global loads for the next stage are issued before the MFMAs.  Token rows of an expert are
-// gathered through perm once per tile.
+// c ^ ((r >> 1) & 7)), so fragment reads are free of bank conflicts.  The global loads of
+// the next stage go straight to LDS (global_load_lds_dwordx4, no staging registers) and
+// are issued before the MFMAs of the current one.  Token rows of an expert are gathered
+// through perm once per tile.
 // Tiles: the shared block first, then the HIT experts in id order; inside a group
 // the token tiles of one weight tile are consecutive (the weight tile is then
 // served from L2), and consecutive tiles are kept on one XCD.
@@ -36,6 +39,7 @@ constexpr int kBT = 256;                       // tokens per tile
 constexpr int kBK = 64;                        // contraction per stage (32 or 64)
 constexpr int kWavesPerEU = kWaveT == 128 ? 1 : 2;  // waves per SIMD the register budget targets
 constexpr int kTS = kWaveT / 16;               // token sub-tiles per wave
+constexpr int kTStride = 16 * (kBT / kWaveT);  // tile rows between a wave's token sub-tiles
 constexpr int kXcdBlocks = 32;                 // blocks one XCD runs at a time (32 CUs, 1 block each)
 constexpr int kRowBytes = kBK * 2;             // bytes of a staged row
 constexpr int kCPR = kBK / 8;                  // 16-byte chunks per staged row
@@ -45,7 +49,6 @@ constexpr int kRowStep = kThreads / kCPR;      // staging rows between a thread'
 constexpr int kWChunks = kBM * kCPR / kThreads;  // 16-byte weight chunks per thread per stage
 constexpr int kXChunks = kBT * kCPR / kThreads;  // 16-byte token chunks per thread per stage
 constexpr int kUpFeat = kBM / 2;               // features of an up tile (W1 rows = W3 rows)
-constexpr int kPrefetch = 1;                   // stages of global loads in flight (1 or 2)
 static_assert(kBK == 32 || kBK == 64, "a stage is one or two MFMA k-steps");
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
@@ -205,6 +208,15 @@ __device__ __forceinline__ uint32_t lds_off(int r, int c) {
     return (uint32_t)(r * kRowBytes + ((c ^ sw) << 4));
 }
 
+// 16 bytes from this lane's global address to LDS byte lds + 16 * lane, for an lds address
+// uniform over the wave (global_load_lds_dwordx4; counted by vmcnt, not lgkmcnt).  Device
+// pass only: the host pass of a kernel naming this target builtin would lose its launch stub.
+__device__ __forceinline__ void load_lds16(const void* g, void* lds) {
+#if defined(__HIP_DEVICE_COMPILE__)
+    __builtin_amdgcn_global_load_lds(g, lds, 16, 0, 0);
+#endif
+}
+
 template <bool kUp>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWavesPerEU))) void expert_gemm_kernel(
     GemmArgs a) {
@@ -214,14 +226,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
     if (!resolve<kUp>(a, xcd_tile(blockIdx.x, gridDim.x), j, s_scan)) return;
 
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-    const int wf = w & 1, wt = w >> 1;  // wave's feature half and token block of the tile
+    // wave's feature half and token lane group: token sub-tile t of the wave holds the tile's
+    // rows kTStride t + 16 wt .. + 15, so a ragged last tile spreads over the SIMDs
+    const int wf = w & 1, wt = __builtin_amdgcn_readfirstlane(w >> 1);
     const int m = lane & 15, quad = lane >> 4;
 
-    // Staging: this thread moves chunk c16 = tid % kCPR of rows r0 + kRowStep i.  Weight
-    // rows step by a constant, so one 32-bit element offset (from the group's uniform
-    // base pointer) and uniform deltas address them; token rows are gathered.
-    const int c16 = tid % kCPR, r0 = tid / kCPR;
+    // Staging: a wave's direct load (global_load_lds_dwordx4) writes 64 x 16 bytes to
+    // consecutive LDS: 8 staged rows of 8 chunks.  Lane l fills LDS chunk l % 8 of row
+    // r0 = tid / kCPR (+ kRowStep i), which holds the row's chunk (l % 8) ^ swizzle(row),
+    // so that is the chunk it fetches.  Weight rows step by a constant, so one 32-bit element
+    // offset (from the group's uniform base pointer) and uniform deltas address them; token
+    // rows are gathered.
+    const int r0 = tid / kCPR;
     static_assert(kRowStep % 16 == 0 && kUpFeat % kRowStep == 0, "staging rows keep their swizzle");
+    static_assert(kThreads % 64 == 0 && 64 % kCPR == 0, "a wave stages whole rows");
+    const int c16 = (int)((uint32_t)(lds_off(r0, tid % kCPR) % kRowBytes) >> 4);  // the chunk landing at this lane's slot
     const uint32_t woff0 = (uint32_t)(j.wrow0 + r0) * (uint32_t)j.kdim + c16 * 8;
     auto wrow_delta = [&](int i) -> uint32_t {  // rows between chunk 0 and chunk i (uniform)
         const int r = kRowStep * i;
@@ -264,90 +283,70 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
     // the address with bit 6 flipped.  Weights (A): for `up` the wave's feature
     // sub-tiles 0..3 are W1 rows wf*64 + 16 s and 4..7 the W3 rows kUpFeat + the same.
     const uint32_t fbase = lds_off(kUp ? wf * 64 + m : wf * 128 + m, quad);
-    const uint32_t tbase = kWTile + lds_off(wt * kWaveT + m, quad);
-    const uint32_t sbase = lds_off(r0, c16);
+    const uint32_t tbase = kWTile + lds_off(wt * 16 + m, quad);
+    // token sub-tiles of this wave with a live row; the others issue no MFMA
+    const int nlive = min(kTS, max(0, (j.ntok - j.tok0 - 16 * wt + kTStride - 1) / kTStride));
     auto frag_row = [](int s) { return kUp ? (s & 3) * 16 + (s >> 2) * kUpFeat : s * 16; };
 
-    u32x4_t stg[kPrefetch][kWChunks + kXChunks];
     const int nk = j.kdim / kBK;
-    auto load = [&](int set, int kt) {
+    // Stage kt goes straight from global memory into LDS buffer buf: chunk i of this lane
+    // lands in its wave's 1 KiB run of the chunk's rows (lane l at byte 16 l).
+    auto load = [&](int buf, int kt) {
         const uint32_t o = (uint32_t)kt * kBK, ox = (uint32_t)kt * j.kst;
+        unsigned char* run = s_lds + buf * kStageLds + w * 64 * 16;
 #pragma unroll
         for (int i = 0; i < kWChunks; ++i)
-            stg[set][i] = *reinterpret_cast<const u32x4_t*>(wbase + woff0 + wrow_delta(i) + o);
+            load_lds16(wbase + woff0 + wrow_delta(i) + o, run + i * kRowStep * kRowBytes);
 #pragma unroll
         for (int i = 0; i < kXChunks; ++i)
-            stg[set][kWChunks + i] = *reinterpret_cast<const u32x4_t*>(xbase + xoff[i] + ox);
-    };
-    auto store = [&](int set, int buf) {
-        unsigned char* base = s_lds + buf * kStageLds + sbase;
-#pragma unroll
-        for (int i = 0; i < kWChunks; ++i)
-            *reinterpret_cast<u32x4_t*>(base + i * kRowStep * kRowBytes) = stg[set][i];
-#pragma unroll
-        for (int i = 0; i < kXChunks; ++i)
-            *reinterpret_cast<u32x4_t*>(base + kWTile + i * kRowStep * kRowBytes) = stg[set][kWChunks + i];
+            load_lds16(xbase + xoff[i] + ox, run + kWTile + i * kRowStep * kRowBytes);
     };
     auto compute = [&](int buf) {
         const unsigned char* base = s_lds + buf * kStageLds;
+        // the fragments of both k-steps are requested before the first MFMA, so the LDS
+        // latency is paid once per stage
+        u32x4_t bfr[kBK / 32][kTS], afr[kBK / 32][8];
 #pragma unroll
         for (int ks = 0; ks < kBK / 32; ++ks) {
             const uint32_t kx = ks ? 64u : 0u;
-            // every fragment of the k-step is requested before the first MFMA, so the LDS
-            // latency is paid once per k-step rather than once per A fragment
-            u32x4_t bfr[kTS], afr[8];
 #pragma unroll
             for (int t = 0; t < kTS; ++t)
-                bfr[t] = *reinterpret_cast<const u32x4_t*>(base + ((tbase + t * 16 * kRowBytes) ^ kx));
+                bfr[ks][t] = *reinterpret_cast<const u32x4_t*>(base + ((tbase + t * kTStride * kRowBytes) ^ kx));
 #pragma unroll
             for (int s = 0; s < 8; ++s)
-                afr[s] = *reinterpret_cast<const u32x4_t*>(base + ((fbase + frag_row(s) * kRowBytes) ^ kx));
-            __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-            for (int s = 0; s < 8; ++s)
-#pragma unroll
-                for (int t = 0; t < kTS; ++t)
-                    acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, afr[s]),
-                                                                        __builtin_bit_cast(bf16x8_t, bfr[t]),
-                                                                        acc[s][t], 0, 0, 0);
-            __builtin_amdgcn_sched_barrier(0);
+                afr[ks][s] = *reinterpret_cast<const u32x4_t*>(base + ((fbase + frag_row(s) * kRowBytes) ^ kx));
         }
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_setprio(1);  // favour the wave that is issuing MFMAs
+#pragma unroll
+        for (int ks = 0; ks < kBK / 32; ++ks)
+#pragma unroll
+            for (int t = 0; t < kTS; ++t) {
+                if (t >= nlive) continue;  // no live token in this sub-tile
+#pragma unroll
+                for (int s = 0; s < 8; ++s)
+                    acc[s][t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, afr[ks][s]),
+                                                                        __builtin_bit_cast(bf16x8_t, bfr[ks][t]),
+                                                                        acc[s][t], 0, 0, 0);
+            }
+        __builtin_amdgcn_s_setprio(0);
+        __builtin_amdgcn_sched_barrier(0);
     };
 
-    if constexpr (kPrefetch == 2) {
-        // stage k is computed from LDS buffer k % 2; its global loads were issued two
-        // iterations earlier into register set k % 2
-        load(0, 0);
-        if (nk > 1) load(1, 1);
-        store(0, 0);
+    // The loads of stage kt + 1 run under the MFMAs of stage kt; its LDS buffer was last
+    // read in stage kt - 1, which every wave finished before the previous barrier.
+    load(0, 0);
+    for (int kt = 0; kt < nk; ++kt) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);  // vmcnt(0): this wave's direct loads have landed
         __syncthreads();
-        for (int kt = 0; kt < nk; kt += 2) {
-            if (kt + 2 < nk) load(0, kt + 2);
-            compute(0);
-            if (kt + 1 < nk) store(1, 1);
-            __syncthreads();
-            if (kt + 1 >= nk) break;
-            if (kt + 3 < nk) load(1, kt + 3);
-            compute(1);
-            if (kt + 2 < nk) store(0, 0);
-            __syncthreads();
-        }
-    } else {
-        load(0, 0);
-        store(0, 0);
-        __syncthreads();
-        for (int kt = 0; kt < nk; ++kt) {
-            if (kt + 1 < nk) load(0, kt + 1);
-            compute(kt & 1);
-            if (kt + 1 < nk) store(0, (kt + 1) & 1);
-            __syncthreads();
-        }
+        if (kt + 1 < nk) load((kt + 1) & 1, kt + 1);
+        compute(kt & 1);
     }
 
     // Epilogue: lane holds features 4*quad .. +3 of sub-tile s for token m of sub-tile t.
 #pragma unroll
     for (int t = 0; t < kTS; ++t) {
-        const int pos = j.tok0 + wt * kWaveT + t * 16 + m;
+        const int pos = j.tok0 + t * kTStride + wt * 16 + m;
         if (pos >= j.ntok) continue;
         if (kUp) {
             // intermediates are k-blocked: element (row, f) at ((f / kBK) * rows + row) * kBK + f % kBK,
