@@ -11,10 +11,11 @@
 //   1. route_prefill_kernel: per 16 tokens, the logits as fp64 MFMA tiles of 16 experts x
 //      16 tokens (two waves per tile, each half the contraction), then the tokens' top-K,
 //      gates and classes in the same block, and the block's histogram of bucket keys;
-//   2. bucket_scan_kernel: one block turns the histograms into each key's start (offsets,
-//      work lists, class counts) and each block's running count within every key;
+//   2. bucket_scan_kernel: a wave per bucket key turns its histogram row into each routing
+//      block's running count within the key and the key's total; the last scan block to
+//      finish turns the totals into each key's start (offsets, work lists, class counts);
 //   3. bucket_scatter_kernel: per 16 tokens, the stable positions of their slots (perm,
-//      inv_perm).  The scan block also writes the host copies when asked.
+//      inv_perm).  The last scan block also writes the host copies when asked.
 //
 // bf16 x bf16 and fp32 x fp32 products are exact in fp64, so on every path only the
 // summation order of the logits differs from a plain loop.
@@ -49,19 +50,23 @@ __global__ __launch_bounds__(kBucketThreads) void route_bucket_kernel(RouteArgs 
     if (a.hx || a.h_idx || a.h_w || a.h_cls || a.h_ready) mirror_host<kBucketThreads>(a);
 }
 
-constexpr int kPrefillThreads = 512;  // 8 waves
+constexpr int kPrefillThreads = 1024;  // 16 waves
+constexpr int kGroupTiles = 2;          // expert tiles of 16 per routing wave
 constexpr int kPrefillTok = 16;       // tokens per prefill routing block (one MFMA tile wide)
-constexpr int kScanThreads = 1024;    // bucket_scan_kernel: one thread per bucket key (3N <= 768)
+constexpr int kScanThreads = 1024;    // bucket_scan_kernel: a wave per key; the last block a thread per key
+constexpr int kScanKeys = kScanThreads / 64;  // bucket keys per scan block
 static_assert(3 * SPICE_MAX_EXPERTS <= kScanThreads, "a scan thread per bucket key");
 
 // The prefill histogram table in the workspace's logits region (unused on this path: the
 // top-K reads the logits from LDS): [3N][stride] counts (key-major, one column per routing
-// block), then the [3N] key starts.
+// block), then the [3N] key starts, then [3N] key totals (each row 4-aligned; the whole is
+// under 1 byte per logit byte: (3N + 1) * (T / 16 + 4) + 3N ints against 8 T N bytes).
 __host__ __device__ inline int prefill_hist_stride(int T) { return ((T + kPrefillTok - 1) / kPrefillTok + 3) & ~3; }
 
 struct PrefillLds {
-    // partial logits of the contraction parts: [parts][16 tokens][N], parts x N <= 8 x 64
-    double zp[kPrefillThreads / 64 * kPrefillTok * 64];
+    // partial logits of the contraction parts: [parts][16 tokens][N], with parts x N <=
+    // waves x 16 x kGroupTiles (parts = waves / groups, groups >= N / (16 kGroupTiles))
+    double zp[kPrefillThreads / 64 * 16 * kGroupTiles * kPrefillTok];
     double z[kPrefillTok][SPICE_MAX_EXPERTS];  // logits
     unsigned long long key[kPrefillTok][SPICE_MAX_EXPERTS];  // their order-preserving keys
     int res[SPICE_MAX_EXPERTS];
@@ -69,7 +74,7 @@ struct PrefillLds {
     int hist[3 * SPICE_MAX_EXPERTS];
 };
 
-// The products of up to 4 expert tiles (16 experts each, from tile0) with 16 tokens over
+// The products of up to kGroupTiles expert tiles (16 experts each, from tile0) with 16 tokens over
 // the contraction passes [p0, p1), with v_mfma_f64_16x16x4f64; each pass's x chunk is
 // widened once for all the tiles.  A 16-byte load gives each lane 8 (bf16) or 4 (fp32)
 // consecutive k of one row: lane (m = lane % 16, q = lane / 16) holds row m's elements
@@ -79,32 +84,32 @@ struct PrefillLds {
 // while one multiplies.  d is a multiple of V.
 template <int DT>
 __device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr, int tile0, int ntg,
-                                              int p0, int p1, int lane, f64x4_t (&out)[4]) {
+                                              int p0, int p1, int lane, f64x4_t (&out)[kGroupTiles]) {
     using E = RouteElem<DT>;
     constexpr int V = E::V, es = E::es;
     const int m = lane & 15, q = lane >> 4;
-    const char* wr[4];
+    const char* wr[kGroupTiles];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
+    for (int i = 0; i < kGroupTiles; ++i) {
         const int e = (tile0 + i) * 16 + m;
         wr[i] = static_cast<const char*>(a.wg) + (size_t)(i < ntg && e < a.N ? e : 0) * a.d * es;
     }
-    f64x4_t acc[4][2] = {};
+    f64x4_t acc[kGroupTiles][2] = {};
     // Loads are unconditional, from clamped addresses: rows past N and tokens past T read
     // row 0 / token 0 (finite values whose products land only in dropped outputs), and
     // chunks past d read chunk 0 of the row, whose x is zeroed where it is used.  A select
     // at the load would make every pass wait for the next pass's loads to land.
-    auto load = [&](int p, uint4 (&xb)[2], uint4 (&wb)[4][2]) {
+    auto load = [&](int p, uint4 (&xb)[2], uint4 (&wb)[kGroupTiles][2]) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int k = p * 8 * V + c * 4 * V + q * V;
             const size_t kk = (size_t)(k < a.d ? k : 0) * es;
             xb[c] = *reinterpret_cast<const uint4*>(xr + kk);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) wb[i][c] = *reinterpret_cast<const uint4*>(wr[i] + kk);
+            for (int i = 0; i < kGroupTiles; ++i) wb[i][c] = *reinterpret_cast<const uint4*>(wr[i] + kk);
         }
     };
-    auto mul = [&](int p, const uint4 (&xb)[2], const uint4 (&wb)[4][2]) {
+    auto mul = [&](int p, const uint4 (&xb)[2], const uint4 (&wb)[kGroupTiles][2]) {
 #pragma unroll
         for (int c = 0; c < 2; ++c) {
             const int k = p * 8 * V + c * 4 * V + q * V;
@@ -112,7 +117,7 @@ __device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr
             double xd[V];
             E::widen(k < a.d ? xb[c] : zero, xd);
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
+            for (int i = 0; i < kGroupTiles; ++i) {
                 if (i < ntg) {  // uniform
                     double wd[V];
                     E::widen(wb[i][c], wd);
@@ -124,7 +129,7 @@ __device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr
         }
     };
     if (p0 < p1) {
-        uint4 xa[2], wa[4][2], xb[2], wb[4][2];
+        uint4 xa[2], wa[kGroupTiles][2], xb[2], wb[kGroupTiles][2];
         load(p0, xa, wa);
         int p = p0;
         for (; p + 1 < p1; p += 2) {
@@ -136,7 +141,7 @@ __device__ __forceinline__ void prefill_group(const RouteArgs& a, const char* xr
         if (p < p1) mul(p, xa, wa);
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i) out[i] = acc[i][0] + acc[i][1];
+    for (int i = 0; i < kGroupTiles; ++i) out[i] = acc[i][0] + acc[i][1];
 }
 
 // Prefill routing of tokens [16 b, 16 b + 16): logits, top-K, gates, classes, and the
@@ -156,23 +161,23 @@ __global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArg
     for (int e = tid; e < N; e += kPrefillThreads) L.res[e] = a.resident_slot[e];
     for (int k = tid; k < NK; k += kPrefillThreads) L.hist[k] = 0;
 
-    // logits: the expert tiles in groups of 4; wave w takes group w / parts and contraction
-    // part w % parts (parts = 8 / groups), leaving its partial logits in LDS; then the parts
-    // are summed in order
-    const int ntile = (N + 15) / 16, ngroups = (ntile + 3) / 4, parts = kNW / ngroups;
+    // logits: the expert tiles in groups of kGroupTiles; wave w takes group w / parts and
+    // contraction part w % parts (parts = waves / groups), leaving its partial logits in LDS;
+    // then the parts are summed in order
+    const int ntile = (N + 15) / 16, ngroups = (ntile + kGroupTiles - 1) / kGroupTiles, parts = kNW / ngroups;
     const int npass = (a.d + 8 * RouteElem<DT>::V - 1) / (8 * RouteElem<DT>::V);
     if (w < ngroups * parts) {
         const int g = w / parts, kp = w - g * parts;
-        const int ntg = min(4, ntile - 4 * g);
-        f64x4_t part[4];
-        prefill_group<DT>(a, xr, 4 * g, ntg, kp * npass / parts, (kp + 1) * npass / parts, lane, part);
+        const int ntg = min(kGroupTiles, ntile - kGroupTiles * g);
+        f64x4_t part[kGroupTiles];
+        prefill_group<DT>(a, xr, kGroupTiles * g, ntg, kp * npass / parts, (kp + 1) * npass / parts, lane, part);
         // result layout of the f64 16x16x4 product: element v of lane (m, q) is expert
         // tile*16 + 4v + q for token t0 + m
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+        for (int i = 0; i < kGroupTiles; ++i)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
-                const int ee = (4 * g + i) * 16 + 4 * v + q;
+                const int ee = (kGroupTiles * g + i) * 16 + 4 * v + q;
                 if (i < ntg && ee < N) L.zp[(kp * kPrefillTok + m) * N + ee] = part[i][v];
             }
     }
@@ -188,11 +193,12 @@ __global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArg
     }
     __syncthreads();
 
-    // top-K: wave w ranks tokens w and w + 8 (rank of e = experts with a larger logit, or an
-    // equal one and a smaller id); then its wave takes the gates and classes
+    // top-K: wave w ranks tokens w, w + waves, ... (rank of e = experts with a larger logit,
+    // or an equal one and a smaller id); then its wave takes the gates and classes
     constexpr int kJ = SPICE_MAX_EXPERTS / 64;
+    static_assert(kPrefillTok % kNW == 0, "whole tokens per wave");
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < kPrefillTok / kNW; ++h) {
         const int tt = w + h * kNW;
         const unsigned long long* kr = L.key[tt];
 #pragma unroll
@@ -213,7 +219,7 @@ __global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArg
     __syncthreads();
     // then the block's histogram of bucket keys
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
+    for (int h = 0; h < kPrefillTok / kNW; ++h) {
         const int tt = w + h * kNW, t = t0 + tt;
         if (t < a.T) {
             const float conf_in = (a.conf_mode == SPICE_CONF_INPUT && lane < K) ? a.conf[(size_t)t * K + lane] : 0.f;
@@ -228,42 +234,39 @@ __global__ __launch_bounds__(kPrefillThreads) void route_prefill_kernel(RouteArg
     for (int k = tid; k < NK; k += kPrefillThreads) table[(size_t)k * stride + blockIdx.x] = L.hist[k];
 }
 
-// One block: for each key, the exclusive running count over the routing blocks (in place)
-// and its total; the keys' starts (an exclusive scan over keys in order) to offsets, the
-// table's start row and the work lists; the class counts; then the host copies when asked.
+// Each wave: one key's exclusive running count over the routing blocks (in place) and its
+// total.  The last block to finish: the keys' starts (an exclusive scan over keys in order)
+// to offsets, the table's start row and the work lists; the class counts; then the host
+// copies when asked.
 __global__ __launch_bounds__(kScanThreads) void bucket_scan_kernel(RouteArgs a) {
     __shared__ int s_tot[3 * SPICE_MAX_EXPERTS];
     __shared__ int s_start[3 * SPICE_MAX_EXPERTS];
     __shared__ int s_wsum[kScanThreads / 64];
     __shared__ int s_cls[3];
     __shared__ int s_res[SPICE_MAX_EXPERTS];
-    constexpr int kNW = kScanThreads / 64;
-    constexpr int kGroup = 8;  // rows whose loads one round trip carries
+    __shared__ int s_flag;
+    constexpr int kChunks = 4;  // 256-column spans whose loads one round trip carries
     const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
     const int N = a.N, NK = 3 * N;
     const int nblk = (a.T + kPrefillTok - 1) / kPrefillTok, stride = prefill_hist_stride(a.T);
     int* table = reinterpret_cast<int*>(a.logits_ws);
-    if (tid < 3) s_cls[tid] = 0;
-    const int res = (a.worklist && tid < N) ? a.resident_slot[tid] : -1;  // for the HIT work list
-    // wave w scans the rows of keys w, w + 16, ..., kGroup rows at a time: lane l holds
-    // columns 4l .. 4l+3 of a 256-column span, and a wave-wide inclusive scan gives each
-    // column's exclusive running count
-    for (int g0 = 0; g0 * kNW < NK; g0 += kGroup) {
-        int run[kGroup];
+    int* totals = table + (size_t)(NK + 1) * stride;
+    const int key = blockIdx.x * kScanKeys + w;
+    if (key < NK) {
+        // lane l holds columns 4l .. 4l+3 of each 256-column span, and a wave-wide inclusive
+        // scan gives each column's exclusive running count
+        int* row = table + (size_t)key * stride;
+        int run = 0;
+        for (int c0 = 0; c0 < stride; c0 += kChunks * 256) {
+            int4 v[kChunks];
 #pragma unroll
-        for (int j = 0; j < kGroup; ++j) run[j] = 0;
-        for (int c0 = 0; c0 < stride; c0 += 256) {
-            const int col = c0 + 4 * lane;
-            int4 v[kGroup];
-#pragma unroll
-            for (int j = 0; j < kGroup; ++j) {
-                const int key = w + kNW * (g0 + j);
-                v[j] = (key < NK && col < stride) ? *reinterpret_cast<const int4*>(table + (size_t)key * stride + col)
-                                                  : make_int4(0, 0, 0, 0);
+            for (int j = 0; j < kChunks; ++j) {
+                const int col = c0 + 256 * j + 4 * lane;
+                v[j] = col < stride ? *reinterpret_cast<const int4*>(row + col) : make_int4(0, 0, 0, 0);
             }
 #pragma unroll
-            for (int j = 0; j < kGroup; ++j) {
-                const int key = w + kNW * (g0 + j);
+            for (int j = 0; j < kChunks; ++j) {
+                const int col = c0 + 256 * j + 4 * lane;
                 // columns past the last routing block hold garbage
                 const int x0 = col < nblk ? v[j].x : 0, x1 = col + 1 < nblk ? v[j].y : 0;
                 const int x2 = col + 2 < nblk ? v[j].z : 0, x3 = col + 3 < nblk ? v[j].w : 0;
@@ -274,21 +277,20 @@ __global__ __launch_bounds__(kScanThreads) void bucket_scan_kernel(RouteArgs a) 
                     const int up = __shfl_up(incl, o);
                     if (lane >= o) incl += up;
                 }
-                const int ex = run[j] + incl - mine;
-                if (key < NK && col < stride)
-                    *reinterpret_cast<int4*>(table + (size_t)key * stride + col) =
-                        make_int4(ex, ex + x0, ex + x0 + x1, ex + x0 + x1 + x2);
-                run[j] += __shfl(incl, 63);
+                const int ex = run + incl - mine;
+                if (col < stride)
+                    *reinterpret_cast<int4*>(row + col) = make_int4(ex, ex + x0, ex + x0 + x1, ex + x0 + x1 + x2);
+                run += __shfl(incl, 63);
             }
         }
-#pragma unroll
-        for (int j = 0; j < kGroup; ++j) {
-            const int key = w + kNW * (g0 + j);
-            if (key < NK && lane == 0) s_tot[key] = run[j];
-        }
+        // written through to the device-coherent level for the last block (route_last_block)
+        if (lane == 0) __hip_atomic_store(totals + key, run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    __syncthreads();
-    const int tot = tid < NK ? s_tot[tid] : 0;
+    if (!route_last_block(&a.ctrl[kWordScanCount], gridDim.x, &s_flag)) return;
+    if (tid < 3) s_cls[tid] = 0;
+    const int res = (a.worklist && tid < N) ? a.resident_slot[tid] : -1;  // for the HIT work list
+    const int tot = tid < NK ? __hip_atomic_load(totals + tid, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0;
+    if (tid < NK) s_tot[tid] = tot;
     // exclusive scan of the totals over keys
     int incl = tot;
 #pragma unroll
@@ -394,7 +396,8 @@ hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
             hipLaunchKernelGGL(route_prefill_kernel<SPICE_BF16>, dim3(nb), dim3(kPrefillThreads), 0, s, a);
         else
             hipLaunchKernelGGL(route_prefill_kernel<SPICE_F32>, dim3(nb), dim3(kPrefillThreads), 0, s, a);
-        hipLaunchKernelGGL(bucket_scan_kernel, dim3(1), dim3(kScanThreads), 0, s, a);
+        hipLaunchKernelGGL(bucket_scan_kernel, dim3((unsigned)((3 * a.N + kScanKeys - 1) / kScanKeys)), dim3(kScanThreads),
+                           0, s, a);
         hipLaunchKernelGGL(bucket_scatter_kernel, dim3(nb), dim3(64), 0, s, a);
         return hipGetLastError();
     }

@@ -12,6 +12,7 @@ namespace spice {
 // Workspace control region (32-bit words at the start of every workspace).
 constexpr int kWordFlags = 0;       // device flags, SPICE_FLAG_* (atomic OR)
 constexpr int kWordWorkCount = 16;  // [3] non-empty buckets per class (the work lists' lengths)
+constexpr int kWordScanCount = 32;  // arrivals of the prefill bucket-scan blocks
 constexpr int kWordWorkList = 1024; // [3][N] int4 work records {expert, pool slot, start, n}
 constexpr int kWordTokCount = 4096; // [T] arrivals of a token's routing blocks (T <= kRouteTokenMaxT)
 static_assert(kWordWorkList + 3 * SPICE_MAX_EXPERTS * 4 <= kWordTokCount, "work lists overlap the counters");
