@@ -50,32 +50,58 @@ METRIC = "MoE-layer decode tokens/s + achieved HBM GB/s (% peak), DSV2-Lite-shap
 TRAFFIC_RECORDS = {
     # the layer's GPU path at T = 32: layer_route + layer_up + layer_down + combine
     "layer_bf16": {
-        "kernel_sources": ("paper_2608_21240_amd/csrc/layer_decode.hip", "paper_2608_21240_amd/csrc/route_device.h",
-                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h", "paper_2608_21240_amd/csrc/tile_index.h",
-                           "paper_2608_21240_amd/csrc/combine.hip"),
-        "source_sha256_16": "a78dec8c8d42b2e5",
-        "fetch_kib_per_call": 12042.6 + 184115.6 + 90271.8 + 905.8,
+        "kernel_sources": ("paper_2608_21240_amd/csrc/layer_decode.hip",
+                           "paper_2608_21240_amd/csrc/route_device.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_mx_tiles.h",
+                           "paper_2608_21240_amd/csrc/tile_index.h",
+                           "paper_2608_21240_amd/csrc/combine.hip",
+                           "paper_2608_21240_amd/csrc/spice_internal.h"),
+        "source_sha256_16": "9d6cf5b00b85fd9f",
+        "fetch_kib_per_call": 12026.9 + 184134.5 + 90266.6 + 905.4,
         "write_kib_per_call": 260.1 + 675.8 + 1195.7 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
         "profile": "profiles/layer_dsv2_decode_kernel_trace_counters.md",
     },
+    # the same with the routed experts in MXFP4 (the layer kernels' MX instantiations)
+    "layer_mxfp4": {
+        "kernel_sources": ("paper_2608_21240_amd/csrc/layer_decode.hip",
+                           "paper_2608_21240_amd/csrc/route_device.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_mx_tiles.h",
+                           "paper_2608_21240_amd/csrc/tile_index.h",
+                           "paper_2608_21240_amd/csrc/combine.hip",
+                           "paper_2608_21240_amd/csrc/spice_internal.h"),
+        "source_sha256_16": "9d6cf5b00b85fd9f",
+        "fetch_kib_per_call": 12024.7 + 55328.8 + 26330.3 + 903.1,
+        "write_kib_per_call": 260.0 + 675.9 + 1195.9 + 128.0,
+        "fetch_factor": 2.0,
+        "write_factor": 1.0,
+        "profile": "profiles/ffn_dsv2_decode_T32_mxfp4.md",
+    },
     # the grouped-FFN call alone at T = 32: ffn_up + ffn_down
     "bf16": {
-        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
-                           "paper_2608_21240_amd/csrc/tile_index.h"),
-        "source_sha256_16": "43e1a297d6387968",
-        "fetch_kib_per_call": 189105.5 + 96795.6,
+        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn.hip",
+                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
+                           "paper_2608_21240_amd/csrc/tile_index.h",
+                           "paper_2608_21240_amd/csrc/spice_internal.h"),
+        "source_sha256_16": "f820fc19f1c1a624",
+        "fetch_kib_per_call": 189112.9 + 96796.2,
         "write_kib_per_call": 462.4 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
         "profile": "profiles/layer_dsv2_decode_kernel_trace_counters.md",
     },
     "mxfp4": {
-        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn_mx.hip", "paper_2608_21240_amd/csrc/expert_ffn_tiles.h"),
-        "source_sha256_16": "b9ad1696bd7c26ef",
-        "fetch_kib_per_call": 60295.41 + 32806.65,
-        "write_kib_per_call": 462.62 + 1451.87,
+        "kernel_sources": ("paper_2608_21240_amd/csrc/expert_ffn_mx.hip",
+                           "paper_2608_21240_amd/csrc/expert_ffn_mx_tiles.h",
+                           "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
+                           "paper_2608_21240_amd/csrc/tile_index.h",
+                           "paper_2608_21240_amd/csrc/spice_internal.h"),
+        "source_sha256_16": "3da504e508d33563",
+        "fetch_kib_per_call": 60286.6 + 32797.4,
+        "write_kib_per_call": 462.6 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
         "profile": "profiles/ffn_dsv2_decode_T32_mxfp4.md",
