@@ -391,6 +391,8 @@ def main():
         launch_us, launch_bytes = time_ffn_launches(devs, xs, confs, per_inst, shape, wl, T, args)
         results[T].update(ffn_call_us=launch_us, ffn_call_GBps=launch_bytes / (launch_us * 1e-6) / 1e9,
                           ffn_call_bytes=launch_bytes)
+        # the routing call on its own (inside the layer call it runs in the first launch)
+        results[T].update(route_call_us=time_route_calls(devs, xs, confs, shape, wl, T))
         print(f"[bench] T={T}: {json.dumps(results[T])}", file=sys.stderr, flush=True)
         del run, gruns
 
@@ -430,6 +432,10 @@ def main():
                      "achieved": round(head["ffn_call_GBps"], 1), "frac": round(head["ffn_call_GBps"] / HBM_PEAK_GBS, 4),
                      "avg_launch_us": round(head["ffn_call_us"], 2), "bytes_per_call": int(head["ffn_call_bytes"]),
                      "traffic": recorded_traffic(args.weights)},
+        "route_call": {"kernel": "route_logits_kernel, one launch with the bucketing in its last block "
+                                 "(moe_route_bucket alone, back-to-back calls; the layer call routes inside "
+                                 "layer_route_kernel instead)",
+                       "us_by_batch": {str(T): round(r["route_call_us"], 2) for T, r in results.items()}},
         "host_path": {"exact_ms": round(head["host_exact_ms"], 3), "experts_per_step": round(head["host_exact_experts"], 2),
                       "GBps": round(head["host_exact_GBps"], 1),
                       "note": "exact-miss residual on the host CPU (Eq. 12 M_cpu): bound by host DRAM reads"},
@@ -489,6 +495,31 @@ def time_ffn_launches(devs, xs, confs, per_inst, shape, wl, T, args, reps: int =
     us = float(np.mean([a.elapsed_time(b) for a, b in evs]) * 1e3)
     nbytes = float(np.mean([per_inst[i]["ffn"] for i in range(len(devs))]))
     return us, nbytes
+
+
+def time_route_calls(devs, xs, confs, shape, wl, T, reps: int = 50):
+    """Mean duration (us) of one standalone routing call (moe_route_bucket: logits, top-K,
+    gates, classes, bucketing and work lists, no host copies): one event pair around
+    back-to-back calls that rotate over the layer instances, behind a spin kernel."""
+    import torch
+
+    from paper_2608_21240_amd import layer as LY
+
+    runs = [LY.LayerRun(shape, T, dev.C, tau=wl.tau, wfmt=wl.wfmt) for dev in devs]
+    for i, dev in enumerate(devs):
+        runs[i].route(dev, xs[i], confs[i], T, to_host=False)
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(int(2e7))
+    a.record()
+    for _ in range(reps):
+        for i, dev in enumerate(devs):
+            runs[i].route(dev, xs[i], confs[i], T, to_host=False)
+    b.record()
+    torch.cuda.synchronize()
+    if any(r.flags() != 0 for r in runs):
+        raise RuntimeError("device flags raised during the routing timing")
+    return a.elapsed_time(b) * 1e3 / (reps * len(devs))
 
 
 def calibrate_split(run, dev, shape, T, args):

@@ -1,12 +1,13 @@
 // Router logits, softmax top-K gating, per-slot classification and (class, expert)
 // bucketing (Eq. 1; Sec. 2.1, 4.2, 4.3).  No block waits for another block.
 //
-// T <= kRouteTokenMaxT (decode), two launches:
-//   1. route_logits_kernel: a token's router rows are spread over several blocks (one row
-//      per wave), each summing its logits in fp64; the last of the token's blocks to finish
-//      (an arrival counter per token) takes the token's top-K, gates, confidence and classes;
-//   2. route_bucket_kernel: one block sorts the T*K slots by (class, expert), writes the
-//      work lists and, when asked, the CPU path's host copies and their ready word.
+// T <= kRouteTokenMaxT (decode), one launch (route_logits_kernel): a token's router rows
+//   are spread over several blocks (one row per wave), each summing its logits in fp64; the
+//   last of the token's blocks to finish (an arrival counter per token) takes the token's
+//   top-K, gates, confidence and classes and publishes them, with the slots' bucket keys,
+//   at the device-coherent level; the last of those blocks over all tokens (a second
+//   arrival counter) sorts the T*K slots by (class, expert), writes the work lists and,
+//   when asked, the CPU path's host copies and their ready word.
 // Larger T (prefill), three launches:
 //   1. route_prefill_kernel: per 16 tokens, the logits as fp64 MFMA tiles of 16 experts x
 //      16 tokens (two waves per tile, each half the contraction), then the tokens' top-K,
@@ -27,27 +28,29 @@ namespace spice {
 namespace {
 
 constexpr int kLogitThreads = 256;   // routing logits: 4 waves, kRouteRowsPerWave router rows each
-constexpr int kBucketThreads = 512;  // bucketing block
-constexpr int kBucketCache = 2048;   // slots whose keys stay in LDS while bucketing (LDS <= 64 KiB at N = 256)
+constexpr int kBucketCache = 1024;   // slots whose keys stay in LDS while the last block buckets them
+// LDS of a decode routing block: the top-K scratch, then (in the last block) the bucketing tables
+constexpr size_t kLogitLdsBytes = sizeof(TopkLds) > bucket_lds_bytes(kLogitThreads, SPICE_MAX_EXPERTS, kBucketCache)
+                                      ? sizeof(TopkLds)
+                                      : bucket_lds_bytes(kLogitThreads, SPICE_MAX_EXPERTS, kBucketCache);
 
 typedef double f64x4_t __attribute__((ext_vector_type(4)));
 
 template <int DT>
 __global__ __launch_bounds__(kLogitThreads) void route_logits_kernel(RouteArgs a, int g_per_tok) {
-    __shared__ TopkLds lds;
+    __shared__ __align__(16) int s_lds[kLogitLdsBytes / sizeof(int)];
     __shared__ int s_flag;
     const int t = blockIdx.x / g_per_tok, g = blockIdx.x % g_per_tok;
     const int rows = (kLogitThreads / 64) * kRouteRowsPerWave;
     const int n_rows = a.N + (a.w_sg ? 1 : 0);
     route_logits_rows<DT>(a, t, g * rows, min(n_rows, (g + 1) * rows));
     if (!route_last_block(&a.ctrl[kWordTokCount + t], g_per_tok, &s_flag)) return;
-    block_topk<kLogitThreads, true>(a, t, a.logits_ws + (size_t)t * a.N, lds);
-}
-
-__global__ __launch_bounds__(kBucketThreads) void route_bucket_kernel(RouteArgs a) {
-    extern __shared__ __align__(16) int s_lds[];
-    bucket_slots<kBucketThreads, kBucketCache>(a, s_lds);
-    if (a.hx || a.h_idx || a.h_w || a.h_cls || a.h_ready) mirror_host<kBucketThreads>(a);
+    block_topk<kLogitThreads, true, true>(a, t, a.logits_ws + (size_t)t * a.N, *reinterpret_cast<TopkLds*>(s_lds));
+    // the published top-K outputs and keys of every token are at the device-coherent level
+    // once every token's last block has counted itself here
+    if (!route_last_block(&a.ctrl[kWordRouteDone], a.T, &s_flag)) return;
+    bucket_slots<kLogitThreads, kBucketCache, true>(a, s_lds);
+    if (a.hx || a.h_idx || a.h_w || a.h_cls || a.h_ready) mirror_host<kLogitThreads, true>(a);
 }
 
 constexpr int kPrefillThreads = 1024;  // 16 waves
@@ -399,12 +402,7 @@ hipError_t launch_route_bucket(const RouteArgs& a, hipStream_t s) {
         hipLaunchKernelGGL(bucket_scan_kernel, dim3((unsigned)((3 * a.N + kScanKeys - 1) / kScanKeys)), dim3(kScanThreads),
                            0, s, a);
         hipLaunchKernelGGL(bucket_scatter_kernel, dim3(nb), dim3(64), 0, s, a);
-        return hipGetLastError();
     }
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(route_bucket_kernel, dim3(1), dim3(kBucketThreads),
-                       bucket_lds_bytes(kBucketThreads, a.N, kBucketCache), s, a);
     return hipGetLastError();
 }
 

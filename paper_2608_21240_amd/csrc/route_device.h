@@ -180,7 +180,10 @@ struct TopkLds {
 
 // The gates, confidence and classes of token t's K picks, by one wave: z = its N logits,
 // res = resident_slot, pick = its experts in rank order (all in LDS).  Lane k < K returns
-// its slot's bucket key (class * N + expert), the other lanes -1.
+// its slot's bucket key (class * N + expert), the other lanes -1.  kPublish: the outputs
+// and the key (control word kWordSlotKeys + slot) are written through to the
+// device-coherent level, for a block of the same launch on another XCD.
+template <bool kPublish = false>
 __device__ int wave_topk_gates(const RouteArgs& a, int t, const double* z, const int* res, const int* pick,
                                int lane, float conf_in) {
     constexpr int kJ = SPICE_MAX_EXPERTS / 64;
@@ -211,9 +214,17 @@ __device__ int wave_topk_gates(const RouteArgs& a, int t, const double* z, const
         if (slot >= 0) cls = SPICE_CLASS_HIT;
         else if (conf < a.tau) cls = SPICE_CLASS_LORE;
         else cls = SPICE_CLASS_EXACT;
-        a.topk_idx[s] = my_e;
-        a.topk_w[s] = (float)g;
-        a.slot_class[s] = cls;
+        if (kPublish) {
+            __hip_atomic_store(a.topk_idx + s, my_e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.topk_w + s, (float)g, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.slot_class + s, cls, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(a.ctrl + kWordSlotKeys + s, (uint32_t)(cls * N + my_e), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            a.topk_idx[s] = my_e;
+            a.topk_w[s] = (float)g;
+            a.slot_class[s] = cls;
+        }
         return cls * N + my_e;
     }
     return -1;
@@ -224,8 +235,9 @@ __device__ int wave_topk_gates(const RouteArgs& a, int t, const double* z, const
 // (a larger logit, or an equal one with a smaller id); each wave counts a share of the
 // experts ee against every e, and rank k < K makes e the k-th pick (descending, the lower id
 // wins ties).  Then the softmax over all N, the gate of each pick (its probability,
-// optionally renormalised over the K), its confidence and its class.
-template <int NT, bool kCoherent>
+// optionally renormalised over the K), its confidence and its class (kPublish: see
+// wave_topk_gates).
+template <int NT, bool kCoherent, bool kPublish = false>
 __device__ void block_topk(const RouteArgs& a, int t, const double* zg, TopkLds& L) {
     constexpr int NW = NT / 64;
     constexpr int kJ = SPICE_MAX_EXPERTS / 64;
@@ -265,7 +277,7 @@ __device__ void block_topk(const RouteArgs& a, int t, const double* zg, TopkLds&
     for (int e = tid; e < N; e += NT)
         if (L.rank[e] < K) L.pick[L.rank[e]] = e;
     __syncthreads();
-    if (w == 0) wave_topk_gates(a, t, L.z, L.res, L.pick, lane, conf_in);
+    if (w == 0) wave_topk_gates<kPublish>(a, t, L.z, L.res, L.pick, lane, conf_in);
 }
 
 // The last of a token's routing blocks to finish, found with an arrival counter.  A block's
@@ -298,6 +310,15 @@ __device__ __forceinline__ int route_slot_key(const RouteArgs& a, int s) {
     return c * a.N + e;
 }
 
+// Bucket key of slot s as the bucketing reads it: from the slot's top-K outputs, or, with
+// kCoherentKeys, the key its routing block published in this launch (always valid).
+template <bool kCoherentKeys>
+__device__ __forceinline__ int bucket_key(const RouteArgs& a, int s) {
+    if (kCoherentKeys)
+        return (int)__hip_atomic_load(a.ctrl + kWordSlotKeys + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return route_slot_key(a, s);
+}
+
 // LDS of bucket_slots for NT threads: two [NT/64][3N] int tables, the [3N] key totals, a
 // few words and the key cache of `cache` slots (the keys of up to that many slots stay in
 // LDS between the two passes; more slots are read twice).
@@ -311,8 +332,9 @@ constexpr size_t bucket_lds_bytes(int nt, int n_experts, int cache) {
 // matching.  Writes offsets, perm and inv_perm, the work lists (for class c, record j =
 // {expert, pool slot (HIT) or -1, bucket start, bucket size} of the j-th non-empty bucket
 // of that class in ascending expert order) with their counts, and the class counts to the
-// host copy when a.h_counts is set.
-template <int NT, int kKeyCache>
+// host copy when a.h_counts is set.  kCoherentKeys: the keys come from bucket_key's
+// published words (the routing ran in this launch).
+template <int NT, int kKeyCache, bool kCoherentKeys = false>
 __device__ void bucket_slots(const RouteArgs& a, int* lds) {
     constexpr int kW = NT / 64;
     constexpr int kBatch = 8;  // 64-slot chunks whose keys one round trip reads
@@ -334,7 +356,7 @@ __device__ void bucket_slots(const RouteArgs& a, int* lds) {
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int s = base + 64 * u + lane;
-            key[u] = s < hi ? route_slot_key(a, s) : -1;
+            key[u] = s < hi ? bucket_key<kCoherentKeys>(a, s) : -1;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
@@ -421,7 +443,7 @@ __device__ void bucket_slots(const RouteArgs& a, int* lds) {
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {
             const int s = base0 + 64 * u + lane;
-            keys[u] = s < hi ? (cached ? s_keys[s] : route_slot_key(a, s)) : -1;
+            keys[u] = s < hi ? (cached ? s_keys[s] : bucket_key<kCoherentKeys>(a, s)) : -1;
         }
 #pragma unroll
         for (int u = 0; u < kBatch; ++u) {  // chunks in slot order: ranks stay stable
@@ -454,7 +476,7 @@ __device__ void bucket_slots(const RouteArgs& a, int* lds) {
 // bucket_slots) by one block, then the ready word: every wave waits for its own stores to
 // complete (a system-scope fence) before thread 0 stores a.ready_value, so a host that
 // sees the value also sees every copy.
-template <int NT>
+template <int NT, bool kCoherent = false>
 __device__ void mirror_host(const RouteArgs& a) {
     const int tid = threadIdx.x;
     const int es = a.dtype == SPICE_BF16 ? 2 : 4;
@@ -466,9 +488,15 @@ __device__ void mirror_host(const RouteArgs& a) {
     }
     const int S = a.T * a.K;
     for (int s = tid; s < S; s += NT) {
-        if (a.h_idx) a.h_idx[s] = a.topk_idx[s];
-        if (a.h_w) a.h_w[s] = a.topk_w[s];
-        if (a.h_cls) a.h_cls[s] = a.slot_class[s];
+        if (kCoherent) {  // written in this launch by routing blocks on any XCD
+            if (a.h_idx) a.h_idx[s] = __hip_atomic_load(a.topk_idx + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a.h_w) a.h_w[s] = __hip_atomic_load(a.topk_w + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (a.h_cls) a.h_cls[s] = __hip_atomic_load(a.slot_class + s, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            if (a.h_idx) a.h_idx[s] = a.topk_idx[s];
+            if (a.h_w) a.h_w[s] = a.topk_w[s];
+            if (a.h_cls) a.h_cls[s] = a.slot_class[s];
+        }
     }
     if (a.h_ready) {
         __threadfence_system();
