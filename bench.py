@@ -57,8 +57,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/combine.hip",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "9d6cf5b00b85fd9f",
-        "fetch_kib_per_call": 12026.9 + 184134.5 + 90266.6 + 905.4,
+        "source_sha256_16": "f68900f8e672e106",
+        "fetch_kib_per_call": 12022.6 + 184129.6 + 90266.1 + 905.6,
         "write_kib_per_call": 260.1 + 675.8 + 1195.7 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
@@ -73,9 +73,9 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/combine.hip",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "9d6cf5b00b85fd9f",
-        "fetch_kib_per_call": 12024.7 + 55328.8 + 26330.3 + 903.1,
-        "write_kib_per_call": 260.0 + 675.9 + 1195.9 + 128.0,
+        "source_sha256_16": "f68900f8e672e106",
+        "fetch_kib_per_call": 12021.5 + 55322.4 + 26344.6 + 903.1,
+        "write_kib_per_call": 260.1 + 675.9 + 1195.9 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
         "profile": "profiles/ffn_dsv2_decode_T32_mxfp4.md",
@@ -86,8 +86,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "f820fc19f1c1a624",
-        "fetch_kib_per_call": 189112.9 + 96796.2,
+        "source_sha256_16": "f12d5eb1ac3a655a",
+        "fetch_kib_per_call": 189116.0 + 96796.1,
         "write_kib_per_call": 462.4 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
@@ -99,8 +99,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "3da504e508d33563",
-        "fetch_kib_per_call": 60286.6 + 32797.4,
+        "source_sha256_16": "9c99fba840272839",
+        "fetch_kib_per_call": 60282.9 + 32787.8,
         "write_kib_per_call": 462.6 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
