@@ -17,9 +17,9 @@
 // Both tiles are staged through LDS (two stages, 128 KiB: one block per CU) in
 // 128-byte rows whose 16-byte chunks are XOR-swizzled by row (chunk c of row r at
 // c ^ ((r >> 1) & 7)), so fragment reads are free of bank conflicts.  The global loads of
-// the next stage go straight to LDS (global_load_lds_dwordx4, no staging registers) and
-// are issued before the MFMAs of the current one.  Token rows of an expert are gathered
-// through perm once per tile.
+// the next stage go straight to LDS (global_load_lds_dwordx4, no staging registers), issued
+// before the MFMAs of the current one by waves 0-3 only.  Token rows of an expert are
+// gathered through perm once per tile.
 // Tiles: the shared block first, then the HIT experts in id order; inside a group
 // the token tiles of one weight tile are consecutive (the weight tile is then
 // served from L2), and consecutive tiles are kept on one XCD.
@@ -45,9 +45,10 @@ constexpr int kRowBytes = kBK * 2;             // bytes of a staged row
 constexpr int kCPR = kBK / 8;                  // 16-byte chunks per staged row
 constexpr int kWTile = kBM * kRowBytes;        // weight tile of one stage
 constexpr int kStageLds = (kBM + kBT) * kRowBytes;
-constexpr int kRowStep = kThreads / kCPR;      // staging rows between a thread's chunks
-constexpr int kWChunks = kBM * kCPR / kThreads;  // 16-byte weight chunks per thread per stage
-constexpr int kXChunks = kBT * kCPR / kThreads;  // 16-byte token chunks per thread per stage
+constexpr int kLoaders = kThreads / 2;         // waves 0-3 issue every global load, one per SIMD
+constexpr int kRowStep = kLoaders / kCPR;      // staging rows between a loader's chunks
+constexpr int kWChunks = kBM * kCPR / kLoaders;  // 16-byte weight chunks per loader per stage
+constexpr int kXChunks = kBT * kCPR / kLoaders;  // 16-byte token chunks per loader per stage
 constexpr int kUpFeat = kBM / 2;               // features of an up tile (W1 rows = W3 rows)
 static_assert(kBK == 32 || kBK == 64, "a stage is one or two MFMA k-steps");
 
@@ -231,13 +232,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
     const int wf = w & 1, wt = __builtin_amdgcn_readfirstlane(w >> 1);
     const int m = lane & 15, quad = lane >> 4;
 
-    // Staging: a wave's direct load (global_load_lds_dwordx4) writes 64 x 16 bytes to
-    // consecutive LDS: 8 staged rows of 8 chunks.  Lane l fills LDS chunk l % 8 of row
-    // r0 = tid / kCPR (+ kRowStep i), which holds the row's chunk (l % 8) ^ swizzle(row),
-    // so that is the chunk it fetches.  Weight rows step by a constant, so one 32-bit element
-    // offset (from the group's uniform base pointer) and uniform deltas address them; token
-    // rows are gathered.
-    const int r0 = tid / kCPR;
+    // Staging: waves 0-3 (one per SIMD) issue all of a stage's loads, so waves 4-7 never wait
+    // behind a queue of loads and keep their SIMD's MFMAs going at the start of a stage.  A
+    // wave's direct load (global_load_lds_dwordx4) writes 64 x 16 bytes to consecutive LDS:
+    // 8 staged rows of 8 chunks.  Lane l fills LDS chunk l % 8 of row r0 = tid / kCPR (+
+    // kRowStep i), which holds the row's chunk (l % 8) ^ swizzle(row), so that is the chunk
+    // it fetches.  Weight rows step by a constant, so one 32-bit element offset (from the
+    // group's uniform base pointer) and uniform deltas address them; token rows are gathered.
+    const int r0 = (tid % kLoaders) / kCPR;
+    const bool loader = tid < kLoaders;
     static_assert(kRowStep % 16 == 0 && kUpFeat % kRowStep == 0, "staging rows keep their swizzle");
     static_assert(kThreads % 64 == 0 && 64 % kCPR == 0, "a wave stages whole rows");
     const int c16 = (int)((uint32_t)(lds_off(r0, tid % kCPR) % kRowBytes) >> 4);  // the chunk landing at this lane's slot
@@ -247,26 +250,30 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
         if (kUp && r >= kUpFeat) return (uint32_t)(j.up_off + r - kUpFeat) * (uint32_t)j.kdim;
         return (uint32_t)r * (uint32_t)j.kdim;
     };
-    uint32_t xoff[kXChunks];
+    // element offsets of a loader's token rows, kept in LDS (each loader reads back only its
+    // own) rather than in registers, which the accumulators and fragments fill
+    __shared__ uint32_t s_xoff[kXChunks][kLoaders];
+    if (loader) {
 #pragma unroll
-    for (int i = 0; i < kXChunks; ++i) {
-        // token rows past the group's end read its last row; their outputs are dropped
-        const int pos = min(j.tok0 + r0 + kRowStep * i, j.ntok - 1);
-        int row;
-        if (j.shared) {
-            row = pos;
-        } else if (j.gather) {
-            const int s = a.perm[j.start + pos];
-            if (s < 0 || s >= a.T * a.K) {
-                atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
-                row = 0;
+        for (int i = 0; i < kXChunks; ++i) {
+            // token rows past the group's end read its last row; their outputs are dropped
+            const int pos = min(j.tok0 + r0 + kRowStep * i, j.ntok - 1);
+            int row;
+            if (j.shared) {
+                row = pos;
+            } else if (j.gather) {
+                const int s = a.perm[j.start + pos];
+                if (s < 0 || s >= a.T * a.K) {
+                    atomicOr(&a.ctrl[kWordFlags], (uint32_t)SPICE_FLAG_BAD_INDEX);
+                    row = 0;
+                } else {
+                    row = s / a.K;
+                }
             } else {
-                row = s / a.K;
+                row = j.start + pos;
             }
-        } else {
-            row = j.start + pos;
+            s_xoff[i][tid] = (uint32_t)row * (uint32_t)j.ld + c16 * 8;
         }
-        xoff[i] = (uint32_t)row * (uint32_t)j.ld + c16 * 8;
     }
     const uint16_t* __restrict__ wbase = j.w;
     const uint16_t* __restrict__ xbase = j.act;
@@ -289,17 +296,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kWaves
     auto frag_row = [](int s) { return kUp ? (s & 3) * 16 + (s >> 2) * kUpFeat : s * 16; };
 
     const int nk = j.kdim / kBK;
-    // Stage kt goes straight from global memory into LDS buffer buf: chunk i of this lane
-    // lands in its wave's 1 KiB run of the chunk's rows (lane l at byte 16 l).
-    auto load = [&](int buf, int kt) {
+    // Stage kt goes straight from global memory into LDS buffer buf: chunk i of this loader
+    // lane lands in its wave's 1 KiB run of the chunk's rows (lane l at byte 16 l).
+    auto load = [&](int buf, int kt) {  // loaders only
+        if (!loader) return;
         const uint32_t o = (uint32_t)kt * kBK, ox = (uint32_t)kt * j.kst;
-        unsigned char* run = s_lds + buf * kStageLds + w * 64 * 16;
+        unsigned char* run = s_lds + buf * kStageLds + (w & 3) * 64 * 16;
 #pragma unroll
         for (int i = 0; i < kWChunks; ++i)
             load_lds16(wbase + woff0 + wrow_delta(i) + o, run + i * kRowStep * kRowBytes);
 #pragma unroll
         for (int i = 0; i < kXChunks; ++i)
-            load_lds16(xbase + xoff[i] + ox, run + kWTile + i * kRowStep * kRowBytes);
+            load_lds16(xbase + s_xoff[i][tid] + ox, run + kWTile + i * kRowStep * kRowBytes);
     };
     auto compute = [&](int buf) {
         const unsigned char* base = s_lds + buf * kStageLds;
