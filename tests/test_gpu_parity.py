@@ -251,6 +251,29 @@ def test_host_copies_match_device_outputs(shape, T, R, layer_call):
     assert np.array_equal(to_np(run.x_host[:T]), c.x)
 
 
+# Decode routing of more slots than its bucketing block keeps in LDS (T*K = 2560 > 1024
+# at T = 256, the largest decode batch): that block reads the keys the top-K blocks
+# published twice, once per pass.
+MANY_SLOTS = W.MoEShape(d=200, n_experts=20, top_k=10, inter=104, shared_inter=168, lore_rank=24,
+                        dtype=W.DTYPE_BF16)
+
+
+def test_decode_routing_more_slots_than_the_key_cache():
+    T, R = 256, 8
+    say(f"decode routing d={MANY_SLOTS.d} N={MANY_SLOTS.n_experts} K={MANY_SLOTS.top_k} T={T} R={R}")
+    c = Case(small_wl(MANY_SLOTS, T, R))
+    c.run_gpu(layer_call=False)
+    c.run_oracle()
+    c.check_routing()
+    c.check_outputs()
+    run = c.run
+    assert np.array_equal(run.idx_host[:T].numpy(), c.g["idx"])
+    assert np.array_equal(run.w_host[:T].numpy(), c.g["w"])
+    assert np.array_equal(run.cls_host[:T].numpy(), c.g["cls"])
+    assert run.counts_host.tolist() == np.bincount(c.g["cls"].reshape(-1), minlength=3).tolist()
+    assert (np.bincount(c.g["cls"].reshape(-1), minlength=3) > 0).all()
+
+
 FORCE_FETCH = dict(cpu_bytes_per_s=1e8, cpu_flops_per_s=1e12, pcie_bytes_per_s=1e13, gpu_fixed_s=0.0, margin=0.0)
 
 
