@@ -57,8 +57,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/combine.hip",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "f68900f8e672e106",
-        "fetch_kib_per_call": 12022.6 + 184129.6 + 90266.1 + 905.6,
+        "source_sha256_16": "85a4b3319e438b10",
+        "fetch_kib_per_call": 12031.4 + 184134.4 + 90267.5 + 905.7,
         "write_kib_per_call": 260.1 + 675.8 + 1195.7 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
@@ -73,9 +73,9 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/combine.hip",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "f68900f8e672e106",
-        "fetch_kib_per_call": 12021.5 + 55322.4 + 26344.6 + 903.1,
-        "write_kib_per_call": 260.1 + 675.9 + 1195.9 + 128.0,
+        "source_sha256_16": "85a4b3319e438b10",
+        "fetch_kib_per_call": 12026.7 + 55328.1 + 26318.2 + 903.1,
+        "write_kib_per_call": 260.0 + 675.9 + 1195.9 + 128.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
         "profile": "profiles/ffn_dsv2_decode_T32_mxfp4.md",
@@ -86,8 +86,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "f12d5eb1ac3a655a",
-        "fetch_kib_per_call": 189116.0 + 96796.1,
+        "source_sha256_16": "8ebc4e31dbfbbff5",
+        "fetch_kib_per_call": 189111.0 + 96795.7,
         "write_kib_per_call": 462.4 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,
@@ -99,8 +99,8 @@ TRAFFIC_RECORDS = {
                            "paper_2608_21240_amd/csrc/expert_ffn_tiles.h",
                            "paper_2608_21240_amd/csrc/tile_index.h",
                            "paper_2608_21240_amd/csrc/spice_internal.h"),
-        "source_sha256_16": "9c99fba840272839",
-        "fetch_kib_per_call": 60282.9 + 32787.8,
+        "source_sha256_16": "562f86020ed6b351",
+        "fetch_kib_per_call": 60286.4 + 32786.7,
         "write_kib_per_call": 462.6 + 1452.0,
         "fetch_factor": 2.0,
         "write_factor": 1.0,

@@ -180,7 +180,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         const int t = b / gr.g_per_tok, g = b % gr.g_per_tok;
         constexpr int rows = kWaves * kRouteRowsPerWave;
         route_logits_rows<DT>(r, t, g * rows, min(r.N + (r.w_sg ? 1 : 0), (g + 1) * rows));
-        if (!route_last_block(&r.ctrl[kWordTokCount + t], gr.g_per_tok, &s_flag)) return;
+        if (!route_last_block(&r.ctrl[kWordTokCount + t * kTokCountStride], gr.g_per_tok, &s_flag)) return;
         block_topk<kThreads, true>(r, t, r.logits_ws + (size_t)t * r.N, *reinterpret_cast<TopkLds*>(&red[0][0][0][0]));
         return;
     }

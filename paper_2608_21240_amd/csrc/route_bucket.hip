@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kLogitThreads) void route_logits_kernel(RouteArgs a
     const int rows = (kLogitThreads / 64) * kRouteRowsPerWave;
     const int n_rows = a.N + (a.w_sg ? 1 : 0);
     route_logits_rows<DT>(a, t, g * rows, min(n_rows, (g + 1) * rows));
-    if (!route_last_block(&a.ctrl[kWordTokCount + t], g_per_tok, &s_flag)) return;
+    if (!route_last_block(&a.ctrl[kWordTokCount + t * kTokCountStride], g_per_tok, &s_flag)) return;
     block_topk<kLogitThreads, true, true>(a, t, a.logits_ws + (size_t)t * a.N, *reinterpret_cast<TopkLds*>(s_lds));
     // the published top-K outputs and keys of every token are at the device-coherent level
     // once every token's last block has counted itself here

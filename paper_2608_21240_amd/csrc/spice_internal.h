@@ -15,17 +15,20 @@ constexpr int kWordWorkCount = 16;  // [3] non-empty buckets per class (the work
 constexpr int kWordScanCount = 32;  // arrivals of the prefill bucket-scan blocks
 constexpr int kWordRouteDone = 33;  // arrivals of the tokens' last routing blocks (decode routing call)
 constexpr int kWordWorkList = 1024; // [3][N] int4 work records {expert, pool slot, start, n}
-constexpr int kWordTokCount = 4096; // [T] arrivals of a token's routing blocks (T <= kRouteTokenMaxT)
+// [T] arrivals of a token's routing blocks (T <= kRouteTokenMaxT), each counter alone in a
+// 128-byte line: the atomics of different tokens' blocks do not queue on one line
+constexpr int kWordTokCount = 4096;
+constexpr int kTokCountStride = 32;  // words between two tokens' counters
 static_assert(kWordWorkList + 3 * SPICE_MAX_EXPERTS * 4 <= kWordTokCount, "work lists overlap the counters");
 
 // Largest T whose routing spreads each token's router rows over a few blocks (larger T:
 // the tiled logits kernel).
 constexpr int kRouteTokenMaxT = 256;
-static_assert((kWordTokCount + kRouteTokenMaxT) * 4 <= SPICE_WS_CONTROL_BYTES, "control region too small");
+static_assert((kWordTokCount + kRouteTokenMaxT * kTokCountStride) * 4 <= SPICE_WS_CONTROL_BYTES, "control region too small");
 // [T*K] bucket keys (class * N + expert) of the decode routing call's slots, written through
 // to the device-coherent level for the block that buckets them (top-K of 64 at most)
-constexpr int kWordSlotKeys = 8192;
-static_assert(kWordTokCount + kRouteTokenMaxT <= kWordSlotKeys, "slot keys overlap the counters");
+constexpr int kWordSlotKeys = 12288;
+static_assert(kWordTokCount + kRouteTokenMaxT * kTokCountStride <= kWordSlotKeys, "slot keys overlap the counters");
 static_assert((kWordSlotKeys + kRouteTokenMaxT * 64) * 4 <= SPICE_WS_CONTROL_BYTES, "control region too small");
 // Most slots T*K of the fused decode-layer launches (layer_decode.hip); larger calls take
 // the separate routing, FFN and combine launches.
