@@ -172,7 +172,7 @@ def expert_bytes(wl) -> int:
 
 
 def algorithmic_bytes(shape, idx, cls, e_bytes=None):
-    """Bytes the method must move on the GPU for one layer call (the survey's definition):
+    """Bytes the method must move on the GPU for one layer call, by definition:
     router + shared block + distinct HIT experts x expert bytes + distinct LoRE experts x
     factor bytes + x read + out written.  Skipped non-resident experts and the fp32 scratch
     rows (y_slots, y_shared, H) are not counted.  ffn: the share of the grouped-FFN call
@@ -371,7 +371,7 @@ def main():
         if run.flags() != 0:
             raise RuntimeError("device flags raised during the timed steps")
 
-        # the GPU path alone (the survey's t_gpu)
+        # the GPU path alone: routing to combine on the device stream, the host residual precomputed
         (gpu_us, gpu_med), graph, graph_ok = time_gpu_path(devs, xs, confs, gruns, T, reps=args.gpu_reps)
         graph_us, graph_med = graph if graph else (None, None)
         tot_bytes = float(np.mean([p["total"] for p in per_inst]))
