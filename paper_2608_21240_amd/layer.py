@@ -223,6 +223,10 @@ class LayerRun:
         self.last_host_s = 0.0  # wall time of the last host residual call
         self.last_host_experts = 0  # distinct experts it read
 
+    def _same_format(self, L: DeviceLayer) -> None:
+        if L.wfmt != self.cfg.wfmt:
+            raise ValueError(f"the layer's expert weights are in format {L.wfmt}, the run was made for {self.cfg.wfmt}")
+
     # -- the steps, each one C-ABI call ------------------------------------------------
     def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
               to_host: bool = True):
@@ -243,6 +247,7 @@ class LayerRun:
         records no event after the call (for graph capture)."""
         T = self.T if T is None else T
         ho = None
+        self._same_format(L)
         if to_host:
             self.epoch = (self.epoch + 1) & 0x7FFFFFFF
             self.host_out.ready_value = self.epoch
@@ -258,6 +263,7 @@ class LayerRun:
 
     def experts(self, L: DeviceLayer, x: torch.Tensor, T: Optional[int] = None, fuse_lore: bool = True):
         T = self.T if T is None else T
+        self._same_format(L)
         la, lb = (L.lore_A, L.lore_B) if fuse_lore else (None, None)
         if L.w_sg is not None:
             spice.moe_expert_ffn_grouped_gated(self.cfg, T, x, self.perm, self.offsets, L.resident_slot, L.w13_pool,

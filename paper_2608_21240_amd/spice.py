@@ -164,6 +164,28 @@ def _check(fn: str, st: int) -> None:
         raise SpiceError(fn, st, lib().spice_last_error().decode())
 
 
+def _matrix_bytes(cfg, rows: int, K: int) -> int:
+    """Bytes of one routed-expert matrix [rows][K] in the cfg's weight format (the MXFP4 blob
+    holds rows*K/2 code bytes and rows*K/32 scale bytes)."""
+    if cfg.wfmt == SPICE_WFMT_MXFP4:
+        return rows * K // 2 + rows * K // 32
+    return rows * K * (2 if cfg.dtype == SPICE_BF16 else 4)
+
+
+def _check_pools(fn: str, cfg, w13_pool, w2_pool) -> None:
+    """Reject pool tensors smaller than cfg.n_slots experts in the cfg's weight format (for
+    instance MXFP4 blobs passed with a cfg that says bf16): the kernels index the slots from
+    the cfg alone, so a short pool would be read past its end.  Raw addresses pass unchecked."""
+    for name, buf, rows, K in (("w13_pool", w13_pool, 2 * cfg.inter, cfg.d), ("w2_pool", w2_pool, cfg.d, cfg.inter)):
+        if buf is None or not hasattr(buf, "element_size"):
+            continue
+        need = max(cfg.n_slots, 0) * _matrix_bytes(cfg, rows, K)
+        have = buf.numel() * buf.element_size()
+        if have < need:
+            raise ValueError(f"{fn}: {name} holds {have} bytes, the cfg (n_slots {cfg.n_slots}, wfmt {cfg.wfmt}, "
+                             f"dtype {cfg.dtype}) needs {need}")
+
+
 def last_error() -> str:
     return lib().spice_last_error().decode()
 
@@ -203,6 +225,7 @@ def moe_route_bucket(cfg, T, x, w_gate, logit_bias, resident_slot, conf, logits,
 
 def moe_expert_ffn_grouped(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared,
                            lore_A, lore_B, y_slots, y_shared, ws, ws_bytes, stream=None) -> None:
+    _check_pools("moe_expert_ffn_grouped", cfg, w13_pool, w2_pool)
     _check("moe_expert_ffn_grouped", lib().moe_expert_ffn_grouped(
         ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(resident_slot), _p(w13_pool), _p(w2_pool),
         _p(w13_shared), _p(w2_shared), _p(lore_A), _p(lore_B), _p(y_slots), _p(y_shared), _p(ws), ws_bytes,
@@ -211,6 +234,7 @@ def moe_expert_ffn_grouped(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2
 
 def moe_expert_ffn_grouped_gated(cfg, T, x, perm, offsets, resident_slot, w13_pool, w2_pool, w13_shared, w2_shared,
                                  w_shared_gate, lore_A, lore_B, y_slots, y_shared, ws, ws_bytes, stream=None) -> None:
+    _check_pools("moe_expert_ffn_grouped_gated", cfg, w13_pool, w2_pool)
     _check("moe_expert_ffn_grouped_gated", lib().moe_expert_ffn_grouped_gated(
         ctypes.byref(cfg), T, _p(x), _p(perm), _p(offsets), _p(resident_slot), _p(w13_pool), _p(w2_pool),
         _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(y_slots), _p(y_shared),
@@ -233,6 +257,7 @@ def moe_layer_gpu(cfg, T, x, w_gate, logit_bias, resident_slot, conf, w13_pool, 
                   w_shared_gate, lore_A, lore_B, logits, topk_idx, topk_w, slot_class, offsets, perm, inv_perm,
                   y_slots, y_shared, host_out: Optional[spice_host_out_t], resid, out, ws, ws_bytes,
                   stream=None) -> None:
+    _check_pools("moe_layer_gpu", cfg, w13_pool, w2_pool)
     _check("moe_layer_gpu", lib().moe_layer_gpu(
         ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(w13_pool),
         _p(w2_pool), _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(logits),
@@ -248,6 +273,7 @@ def moe_layer_gpu_noalloc(cfg, T, x, w_gate, logit_bias, resident_slot, conf, w1
                           w2_shared, w_shared_gate, lore_A, lore_B, logits, topk_idx, topk_w, slot_class, offsets,
                           perm, inv_perm, y_slots, y_shared, host_out: Optional[spice_host_out_t], resid, out,
                           stream=None) -> None:
+    _check_pools("moe_layer_gpu_noalloc", cfg, w13_pool, w2_pool)
     _check("moe_layer_gpu_noalloc", lib().moe_layer_gpu_noalloc(
         ctypes.byref(cfg), T, _p(x), _p(w_gate), _p(logit_bias), _p(resident_slot), _p(conf), _p(w13_pool),
         _p(w2_pool), _p(w13_shared), _p(w2_shared), _p(w_shared_gate), _p(lore_A), _p(lore_B), _p(logits),

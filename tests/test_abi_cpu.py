@@ -112,6 +112,29 @@ def test_ffn_lore_combine_validation():
     assert st == spice.SPICE_ERR_INVALID
 
 
+def test_short_pools_are_rejected_by_the_binding():
+    """MXFP4 pool blobs handed over with a cfg that says bf16 are a quarter of the size the
+    kernels would index; the binding refuses them before any library call."""
+    import torch
+
+    s = W.DSV2
+    mx = spice.make_cfg(s, n_slots=2, wfmt=spice.SPICE_WFMT_MXFP4)
+    bf = spice.make_cfg(s, n_slots=2)
+    p13 = torch.empty((2, (2 * s.inter * s.d) * 17 // 32), dtype=torch.uint8)
+    p2 = torch.empty((2, (s.d * s.inter) * 17 // 32), dtype=torch.uint8)
+    spice._check_pools("t", mx, p13, p2)  # the right size for MXFP4
+    with pytest.raises(ValueError, match="w13_pool"):
+        spice.moe_expert_ffn_grouped(bf, 4, DUMMY, DUMMY, DUMMY, DUMMY, p13, p2, DUMMY, DUMMY, None, None, DUMMY,
+                                     DUMMY, DUMMY, 1 << 30)
+    with pytest.raises(ValueError, match="w2_pool"):
+        spice._check_pools("t", mx, p13, p2[:1])
+    three = spice.make_cfg(s, n_slots=3, wfmt=spice.SPICE_WFMT_MXFP4)  # more slots than the pool
+    with pytest.raises(ValueError, match="n_slots 3"):
+        spice.moe_layer_gpu(three, 4, *([DUMMY] * 5), p13, p2, *([DUMMY] * 19), None)
+    bf_pool = torch.empty((2, 2 * s.inter, s.d), dtype=torch.bfloat16)
+    spice._check_pools("t", bf, bf_pool, torch.empty((2, s.d, s.inter), dtype=torch.bfloat16))
+
+
 def test_gated_ffn_validation():
     c = cfg()
     L = spice.lib()
