@@ -69,7 +69,7 @@ class StackModel:
         return SimpleNamespace(wg=self.wg[l], bias=None, resident_slot=self.resident_slot[l],
                                w13_pool=self.w13_pool[l], w2_pool=self.w2_pool[l], w13s=self.w13s, w2s=self.w2s,
                                lore_A=self.lore_A, lore_B=self.lore_B, host_w13=self.w13_host, host_w2=self.w2_host,
-                               w_sg=None)
+                               w_sg=None, wfmt=spice.SPICE_WFMT_DTYPE)
 
 
 class StackRun:
