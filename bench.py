@@ -500,7 +500,8 @@ def time_ffn_launches(devs, xs, confs, per_inst, shape, wl, T, args, reps: int =
 def time_route_calls(devs, xs, confs, shape, wl, T, reps: int = 50):
     """Mean duration (us) of one standalone routing call (moe_route_bucket: logits, top-K,
     gates, classes, bucketing and work lists, no host copies): one event pair around
-    back-to-back calls that rotate over the layer instances, behind a spin kernel."""
+    back-to-back calls that rotate over the layer instances, behind a spin kernel, with no
+    event recorded between the calls."""
     import torch
 
     from paper_2608_21240_amd import layer as LY
@@ -514,7 +515,7 @@ def time_route_calls(devs, xs, confs, shape, wl, T, reps: int = 50):
     a.record()
     for _ in range(reps):
         for i, dev in enumerate(devs):
-            runs[i].route(dev, xs[i], confs[i], T, to_host=False)
+            runs[i].route(dev, xs[i], confs[i], T, to_host=False, mark=False)
     b.record()
     torch.cuda.synchronize()
     if any(r.flags() != 0 for r in runs):
@@ -764,13 +765,14 @@ def prefill_main(args):
     ffn_ms = np.array([e["routed"].elapsed_time(e["experts"]) for e in evs])
     route_event_us = float(np.median([e["start"].elapsed_time(e["routed"]) for e in evs]) * 1e3)
     # the routing alone: average over back-to-back calls from one event pair behind a spin
-    # kernel (a per-call event pair also holds the host's submission of the call)
+    # kernel and no event between the calls (a per-call event pair also holds the host's
+    # submission of the call)
     reps = 30
     ra, rb = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda._sleep(int(2e7))
     ra.record()
     for _ in range(reps):
-        run.route(dev, x, conf, T, to_host=False)
+        run.route(dev, x, conf, T, to_host=False, mark=False)
     rb.record()
     torch.cuda.synchronize()
     route_us = ra.elapsed_time(rb) * 1e3 / reps

@@ -229,14 +229,16 @@ class LayerRun:
 
     # -- the steps, each one C-ABI call ------------------------------------------------
     def route(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
-              to_host: bool = True):
-        """Routing + bucketing; with to_host the kernel also fills the pinned host copies,
-        and e_route marks the end of the call on the stream."""
+              to_host: bool = True, mark: bool = True):
+        """Routing + bucketing; with to_host the kernel also fills the pinned host copies.
+        e_route marks the end of the call on the stream (mark=False records no event, for
+        back-to-back timing; the host then has nothing to wait on)."""
         T = self.T if T is None else T
         spice.moe_route_bucket(self.cfg, T, x, L.wg, L.bias, L.resident_slot, conf, self.logits, self.topk_idx,
                                self.topk_w, self.slot_class, self.offsets, self.perm, self.inv_perm,
                                self.host_out_ev if to_host else None, self.ws, self.ws_bytes)
-        self.e_route.record(torch.cuda.current_stream())
+        if mark:
+            self.e_route.record(torch.cuda.current_stream())
         self.wait_ready = False
 
     def layer_gpu(self, L: DeviceLayer, x: torch.Tensor, conf: Optional[torch.Tensor], T: Optional[int] = None,
