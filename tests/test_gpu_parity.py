@@ -77,6 +77,35 @@ def test_ragged_layers(shape, T, R, layer_call):
         check_combine_in_layer_call(c)
 
 
+# A shape the prefill GEMMs never take (d not a multiple of 256), and one they take from
+# 256 tokens on.
+LIMIT_STREAM = W.MoEShape(d=264, n_experts=16, top_k=8, inter=136, shared_inter=200, lore_rank=8,
+                          dtype=W.DTYPE_BF16)
+LIMIT_GEMM = W.MoEShape(d=256, n_experts=16, top_k=4, inter=256, shared_inter=384, lore_rank=16,
+                        dtype=W.DTYPE_BF16)
+
+
+@pytest.mark.parametrize("shape,T,R", [
+    (LIMIT_STREAM, 128, 6),   # T*K = 1024: the largest call of the three fused launches
+    (LIMIT_STREAM, 129, 6),   # 1032 slots: separate routing (decode kernel) and FFN launches
+    (LIMIT_GEMM, 255, 7),     # 1020 slots, below the GEMMs' 256 tokens: fused launches
+    (LIMIT_GEMM, 256, 7),     # 1024 slots, but the GEMMs apply: decode routing, then the GEMMs
+    (LIMIT_GEMM, 257, 7),     # past the decode routing's 256 tokens: prefill routing and GEMMs
+], ids=["stream-1024", "stream-1032", "gemm-T255", "gemm-T256", "gemm-T257"])
+def test_layer_call_at_its_dispatch_limits(shape, T, R):
+    """moe_layer_gpu on either side of each limit that picks its launches (slots of the fused
+    launches, tokens of the decode routing, tokens of the prefill GEMMs): every token's
+    routing and outputs against the oracle."""
+    say(f"layer-call limits d={shape.d} K={shape.top_k} T={T} R={R}")
+    c = Case(small_wl(shape, T, R))
+    c.run_gpu(layer_call=True)
+    c.run_oracle()
+    c.check_routing()
+    c.check_outputs()
+    assert (np.bincount(c.o["cls"].reshape(-1), minlength=3) > 0).all()  # all three classes
+    check_combine_in_layer_call(c)
+
+
 @pytest.fixture(scope="module")
 def dsv2():
     wl = W.WORKLOADS["dsv2_decode_t32"]
